@@ -1,0 +1,220 @@
+/*
+ * kvstate.h - C ABI of the MI355X (gfx950) KV-state library.
+ *
+ * The library implements, on one GPU, the on-device path of the stateful KV
+ * operators of AAFLOW+ (arXiv 2607.10987): a paged, refcounted KV block pool
+ * and the operators materialize, fork, compose (restricted merge), pack /
+ * unpack (the device side of transfer), attend (resume: append-prefill and
+ * decode) and evict.
+ *
+ * Conventions
+ * -----------
+ * - Every function returns a kv_status (KV_OK = 0, errors < 0).
+ * - Host-detectable errors return before anything is enqueued and leave the
+ *   pool unchanged (all-or-nothing).
+ * - Device work is enqueued on `stream` (a hipStream_t passed as void*; NULL
+ *   is the default stream).  All mutating calls on one pool must use one
+ *   stream (or be ordered by the caller); concurrent calls on one pool race.
+ *   kv_release and kv_evict synchronise `stream` before returning.
+ * - The caller owns all device memory: the pool, the metadata area, the
+ *   scratch area, weights, inputs, outputs and transfer buffers.  Device
+ *   pointers must be 256-byte aligned.  The library owns only host-side
+ *   catalog memory.
+ * - Layouts are row-major.  `dtype` is KV_DTYPE_F32 (float) or KV_DTYPE_BF16
+ *   (bfloat16); inputs, weights, outputs and pool contents all use it.
+ *
+ * Pool layout: pool[P][L][2][Hkv][B][dh] (block, layer, K|V, KV head, slot,
+ * channel).  One block holds B consecutive token positions of one state for
+ * every layer (the paper's block b_j = (K_j, V_j, l_j, r_j, d_j), stateful
+ * operator section, with l_j spanning all layers of one physical block).
+ */
+#ifndef KVSTATE_H
+#define KVSTATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t kv_status;
+enum {
+  KV_OK = 0,
+  KV_ERR_ARG = -1,          /* malformed argument */
+  KV_ERR_OOM = -2,          /* not enough free blocks (nothing allocated) */
+  KV_ERR_INCOMPATIBLE = -3, /* Compat(S_a, S_b) = 0: caller should recompute */
+  KV_ERR_EVICTED = -4,      /* handle is stale: evicted or released */
+  KV_ERR_BAD_HEADER = -5,   /* pack header magic/version/sizes invalid */
+  KV_ERR_BUFSIZE = -6,      /* caller buffer too small */
+  KV_ERR_CAPACITY = -7,     /* catalog full or positions beyond max_pos */
+  KV_ERR_HIP = -8,          /* HIP runtime error */
+  KV_ERR_INTERNAL = -9      /* device consistency check failed */
+};
+
+enum { KV_DTYPE_F32 = 0, KV_DTYPE_BF16 = 1 };
+
+/* Lineage word (the paper's Lambda): kind in bits 56..63, fork index j in
+ * bits 32..55, parent state id in bits 0..31 (0xFFFFFFFF = none). */
+enum {
+  KV_LINEAGE_MATERIALIZE = 1,
+  KV_LINEAGE_FORK = 2,
+  KV_LINEAGE_TRANSFER = 3,
+  KV_LINEAGE_MERGE = 4
+};
+
+enum { KV_MAX_BATCH = 64, KV_MAX_SEGMENTS = 64, KV_MAX_FORK = 64 };
+
+typedef int64_t kv_state;       /* catalog slot | generation << 32 */
+typedef struct kv_pool kv_pool; /* opaque */
+typedef void* kv_stream;        /* hipStream_t */
+
+/* Model identity and configuration: the paper's M (model_id) and Theta. Two
+ * states or a pool and a pack header are compatible iff model_id and every
+ * shape field from n_layers to rope_base are equal (Compat predicate, KV state
+ * object section).  max_pos and max_states are capacities of one pool. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, block_size;
+  int32_t dtype;      /* KV_DTYPE_* */
+  int32_t max_pos;    /* positions 0 .. max_pos-1 are valid */
+  int32_t max_states; /* live states in the catalog */
+  int32_t reserved;
+  double rope_base;
+  uint64_t model_id;
+} kv_model_cfg;
+
+/* One segment of a composition: tokens [tok_begin, tok_end) of `state`. */
+typedef struct {
+  kv_state state;
+  int64_t tok_begin, tok_end;
+} kv_segment;
+
+#define KV_PACK_MAGIC 0x5453564Bu
+#define KV_PACK_VERSION 1u
+
+/* Metadata descriptor sent beside a packed payload (KV-Transfer algorithm:
+ * metadata travels separately from the raw block buffers).  Plain old data. */
+typedef struct {
+  uint32_t magic, version;
+  uint64_t model_id;
+  kv_model_cfg cfg;
+  int64_t pos_begin;     /* position of the first packed token */
+  int64_t n_tokens;      /* valid tokens in the payload */
+  int64_t blk_begin;     /* first logical block of the source state */
+  int64_t n_blocks;
+  uint64_t block_bytes;  /* bytes of one block (all layers) */
+  uint64_t payload_bytes;
+  uint64_t lineage;      /* source state's lineage word */
+  int64_t src_state_id;  /* source state's id */
+} kv_pack_header;
+
+/* Sizes of the caller-provided device areas for a pool of n_blocks blocks.
+ * pool_bytes: the block storage; meta_bytes: refcounts, free ring, block
+ * tables, the RoPE table and command staging. */
+kv_status kv_pool_bytes(const kv_model_cfg* cfg, int64_t n_blocks, size_t* pool_bytes,
+                        size_t* meta_bytes);
+
+/* Scratch bytes that let a single materialize/attend call of `tokens` total
+ * new tokens (batch * T) over at most `max_keys` keys per state run with all
+ * layers at once.  A smaller scratch area works: layers are then processed
+ * in groups (at least one layer must fit). */
+size_t kv_scratch_bytes(const kv_model_cfg* cfg, int64_t tokens, int32_t batch,
+                        int64_t max_keys);
+
+/* Create a pool.  init_free_order (host, nullable) is a permutation of
+ * 0..n_blocks-1 giving the initial order of the free ring (default identity).
+ * Builds the cos/sin table (double precision, stored as float) and clears the
+ * metadata; synchronises `stream`. */
+kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_dev,
+                         void* meta_dev, void* scratch_dev, size_t scratch_bytes,
+                         const int32_t* init_free_order, kv_stream stream, kv_pool** out);
+kv_status kv_pool_destroy(kv_pool* pool);
+
+/* Borrow the QKV weights: layer l at w_dev + l * layer_stride_elems, each
+ * [(Hq + 2 Hkv) * dh][d_model] (query heads, then key heads, then value heads;
+ * QKV = X W^T).  The memory must outlive its use. */
+kv_status kv_set_weights(kv_pool* pool, const void* w_dev, int64_t layer_stride_elems);
+
+/* KV-Materialize (KV operator algorithms): prefill x [T][d_model] (one hidden
+ * state matrix shared by every layer) at positions pos0 .. pos0+T-1.  Projects
+ * Q, K, V per layer, applies RoPE to Q and K, writes K and V into newly
+ * allocated blocks (FIFO order), and writes the causal GQA attention output
+ * o [L][T][Hq * dh].  Returns the new state. */
+kv_status kv_materialize(kv_pool* pool, const void* x_dev, int64_t T, int64_t pos0,
+                         void* o_dev, kv_stream stream, kv_state* out);
+
+/* KV-Fork: k children alias every block of `parent` (refcount += k); each
+ * child's lineage records fork(j), j = 1..k.  children: host array of k. */
+kv_status kv_fork(kv_pool* pool, kv_state parent, int32_t k, kv_state* children,
+                  kv_stream stream);
+
+/* Restricted-KV-Merge by ordered, non-overlapping concatenation: segment i is
+ * placed after segments 0..i-1, starting at the position of segment 0's first
+ * token.  Keys of a segment whose position changes by D are re-rotated by D;
+ * values are copied bit-exactly; destination blocks that are identical to a
+ * source block (zero shift, same slot alignment) are aliased instead of
+ * copied.  segs: host array of n (1 <= n <= KV_MAX_SEGMENTS). */
+kv_status kv_compose(kv_pool* pool, const kv_segment* segs, int32_t n, kv_stream stream,
+                     kv_state* out);
+
+/* KV-Transfer, source side: write logical blocks [blk_begin, blk_end) of
+ * `state` to dst_dev as n_blocks * block_bytes contiguous bytes in logical
+ * order (each block in the pool's block layout; slots after the state's last
+ * token zero-filled) and fill *hdr_out. */
+kv_status kv_pack(kv_pool* pool, kv_state state, int64_t blk_begin, int64_t blk_end,
+                  void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream);
+
+/* KV-Transfer, destination side: check the header (KV_ERR_BAD_HEADER) and
+ * compatibility (KV_ERR_INCOMPATIBLE), allocate n_blocks blocks from the free
+ * ring, copy the payload and register a state at positions pos_begin .. */
+kv_status kv_unpack(kv_pool* pool, const kv_pack_header* hdr, const void* src_dev,
+                    size_t src_bytes, kv_stream stream, kv_state* out);
+
+/* KV-Resume over a batch (append-prefill when T > 1, decode when T = 1): for
+ * each state in order, copy-on-write a shared partial tail block, allocate the
+ * blocks the append needs, project x [batch][T][d_model] at positions
+ * pos0+n .. pos0+n+T-1, store K/V, and write the causal attention of the T
+ * new queries over all n+T keys to o [L][batch][T][Hq * dh]. */
+kv_status kv_attend(kv_pool* pool, const kv_state* states, int32_t batch, const void* x_dev,
+                    int64_t T, void* o_dev, kv_stream stream);
+
+/* KV-Evict: order unpinned live states by score = alpha*reuse - beta*size -
+ * gamma*age (ties by state id, ascending), and release them in that order
+ * while allocated blocks > max_allocated_blocks.  LRU is (0, 0, 1).  Blocks
+ * still referenced by another state survive.  Synchronous; *n_evicted is the
+ * number of states evicted. */
+kv_status kv_evict(kv_pool* pool, int64_t max_allocated_blocks, double alpha, double beta,
+                   double gamma, kv_stream stream, int32_t* n_evicted);
+
+/* Drop a state's block references (blocks reaching refcount 0 return to the
+ * tail of the free ring, in logical order).  Synchronous. */
+kv_status kv_release(kv_pool* pool, kv_state state, kv_stream stream);
+
+/* Exclude (pinned != 0) or re-admit a state as an eviction candidate. */
+kv_status kv_pin(kv_pool* pool, kv_state state, int32_t pinned);
+
+/* Wait for the pool's work on `stream`; returns the device's sticky status
+ * (KV_ERR_INTERNAL if a device consistency check failed) and clears it. */
+kv_status kv_sync(kv_pool* pool, kv_stream stream);
+
+/* Catalog queries. */
+kv_status kv_state_info(kv_pool* pool, kv_state state, int64_t* pos0, int64_t* n_tokens,
+                        int64_t* n_blocks, uint64_t* lineage, int64_t* state_id);
+kv_status kv_pool_counts(kv_pool* pool, int64_t* free_blocks, int64_t* live_states,
+                         int64_t* clock);
+
+/* Device-side metadata read back (synchronises `stream`): a state's block
+ * table (host_out must hold n_blocks entries) and the allocator (refcount and
+ * ring arrays of n_blocks entries each, ring head/tail counters). */
+kv_status kv_read_block_table(kv_pool* pool, kv_state state, int32_t* host_out, int64_t cap,
+                              kv_stream stream);
+kv_status kv_read_allocator(kv_pool* pool, int32_t* refcount_out, int32_t* ring_out,
+                            int64_t* head, int64_t* tail, kv_stream stream);
+
+/* Human-readable name of a status. */
+const char* kv_strerror(kv_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KVSTATE_H */

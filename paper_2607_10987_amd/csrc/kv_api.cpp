@@ -1,0 +1,810 @@
+// Host side of the KV-state library: the catalog of states (the paper's
+// S_KV = (M, Theta, B, Pi, Lambda, Gamma) with the metadata-catalog fields
+// state_id, model_id, position_range, block_id, lineage, refcount,
+// last_access), argument and compatibility checks, and the C ABI declared in
+// kvstate.h.  Block ids, refcounts and the free ring live on the device; the
+// host knows the exact number of free blocks (allocations are counted here,
+// releases report their frees back), so every out-of-memory condition is
+// detected before anything is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "kv_internal.h"
+#include "kv_fast.h"
+
+using namespace kvs;
+
+namespace {
+
+constexpr uint32_t kNoParent = 0xFFFFFFFFu;
+
+enum : int32_t { ST_FREE = 0, ST_ACTIVE = 1, ST_EVICTED = 2, ST_RELEASED = 3 };
+
+struct StateRec {
+  uint32_t gen = 0;
+  int32_t status = ST_FREE;
+  int64_t sid = -1;
+  int64_t pos0 = 0, n = 0, nblocks = 0;
+  uint64_t lineage = 0;
+  bool pinned = false;
+  int64_t last_access = 0, reuse = 0;
+  int32_t group = -1;  // tail group of a partial tail block, -1 if none
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+uint64_t lineage_word(uint64_t kind, uint64_t parent, uint64_t j) {
+  return (kind << 56) | ((j & 0xFFFFFFull) << 32) | (parent & 0xFFFFFFFFull);
+}
+
+struct MetaLayout {
+  size_t hdr, rc, ring, tables, rope_cos, rope_sin, cow, cmd, total;
+};
+
+MetaLayout meta_layout(const kv_model_cfg& c, int64_t P) {
+  MetaLayout m;
+  const int64_t max_blocks = ceil_div(c.max_pos, c.block_size);
+  size_t off = 0;
+  m.hdr = off;
+  off += sizeof(DevHeader);
+  m.rc = off;
+  off = align256(off + P * 4);
+  m.ring = off;
+  off = align256(off + P * 4);
+  m.tables = off;
+  off = align256(off + (size_t)c.max_states * max_blocks * 4);
+  m.rope_cos = off;
+  off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
+  m.rope_sin = off;
+  off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
+  m.cow = off;
+  off = align256(off + KV_MAX_BATCH * sizeof(int2));
+  m.cmd = off;
+  off = align256(off + (size_t)c.max_states * 2 * 4);
+  m.total = off;
+  return m;
+}
+
+int elt_bytes(const kv_model_cfg& c) { return c.dtype == KV_DTYPE_BF16 ? 2 : 4; }
+
+bool same_theta(const kv_model_cfg& a, const kv_model_cfg& b) {
+  return a.n_layers == b.n_layers && a.d_model == b.d_model && a.n_q_heads == b.n_q_heads &&
+         a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim &&
+         a.block_size == b.block_size && a.dtype == b.dtype && a.rope_base == b.rope_base;
+}
+
+kv_status check_cfg(const kv_model_cfg* c) {
+  if (!c) return KV_ERR_ARG;
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return KV_ERR_ARG;
+  if (c->n_q_heads % c->n_kv_heads) return KV_ERR_ARG;
+  if (c->head_dim < 16 || c->head_dim > 256 || c->head_dim % 16) return KV_ERR_ARG;
+  if (c->block_size < 1 || c->block_size > 64) return KV_ERR_ARG;
+  if (c->dtype != KV_DTYPE_F32 && c->dtype != KV_DTYPE_BF16) return KV_ERR_ARG;
+  if (c->max_pos < 1 || c->max_states < 1) return KV_ERR_ARG;
+  if (!(c->rope_base > 1.0) || !std::isfinite(c->rope_base)) return KV_ERR_ARG;
+  return KV_OK;
+}
+
+}  // namespace
+
+struct kv_pool {
+  kv_model_cfg cfg;
+  int64_t P = 0;
+  int32_t max_blocks = 0;
+  char* pool = nullptr;
+  char* meta = nullptr;
+  char* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  MetaLayout ml;
+  DevHeader* dhdr = nullptr;
+  int32_t* rc = nullptr;
+  int32_t* ring = nullptr;
+  int32_t* tables = nullptr;
+  float* rope_cos = nullptr;
+  float* rope_sin = nullptr;
+  int2* cow = nullptr;
+  int32_t* cmd = nullptr;
+  int64_t head = 0, tail = 0;  // exact mirror of the device counters
+  std::vector<StateRec> slots;
+  int64_t next_sid = 0;
+  int64_t clock = 0;
+  std::vector<int32_t> holders;  // tail groups: number of states sharing the tail block
+  std::vector<int32_t> free_groups;
+  const void* w = nullptr;
+  int64_t w_stride = 0;
+
+  PoolGeom geom() const {
+    PoolGeom g;
+    g.pool = pool;
+    g.tables = tables;
+    g.rope_cos = rope_cos;
+    g.rope_sin = rope_sin;
+    g.block_elems = (int64_t)cfg.n_layers * 2 * cfg.n_kv_heads * cfg.block_size * cfg.head_dim;
+    g.max_blocks = max_blocks;
+    g.L = cfg.n_layers;
+    g.Hq = cfg.n_q_heads;
+    g.Hkv = cfg.n_kv_heads;
+    g.dh = cfg.head_dim;
+    g.B = cfg.block_size;
+    g.d = cfg.d_model;
+    g.max_pos = cfg.max_pos;
+    return g;
+  }
+  int64_t free_blocks() const { return tail - head; }
+  int64_t live() const {
+    int64_t n = 0;
+    for (const auto& s : slots) n += s.status == ST_ACTIVE;
+    return n;
+  }
+  int32_t new_group(int32_t h) {
+    int32_t g;
+    if (!free_groups.empty()) {
+      g = free_groups.back();
+      free_groups.pop_back();
+      holders[g] = h;
+    } else {
+      g = (int32_t)holders.size();
+      holders.push_back(h);
+    }
+    return g;
+  }
+  void leave_group(StateRec& s) {
+    if (s.group >= 0 && --holders[s.group] == 0) free_groups.push_back(s.group);
+    s.group = -1;
+  }
+  void touch(StateRec& s, bool input) {
+    s.last_access = ++clock;
+    if (input) ++s.reuse;
+  }
+  // a free catalog slot, or -1
+  int32_t take_slot() {
+    for (size_t i = 0; i < slots.size(); ++i)
+      if (slots[i].status != ST_ACTIVE) return (int32_t)i;
+    return -1;
+  }
+  StateRec& open_state(int32_t slot, int64_t pos0, int64_t n, int64_t nblocks, uint64_t lin) {
+    StateRec& s = slots[slot];
+    s.gen += 1;
+    s.status = ST_ACTIVE;
+    s.sid = next_sid++;
+    s.pos0 = pos0;
+    s.n = n;
+    s.nblocks = nblocks;
+    s.lineage = lin;
+    s.pinned = false;
+    s.last_access = 0;
+    s.reuse = 0;
+    s.group = -1;
+    return s;
+  }
+  kv_state handle(int32_t slot) const {
+    return (kv_state)(uint32_t)slot | ((kv_state)slots[slot].gen << 32);
+  }
+  kv_status lookup(kv_state h, int32_t* slot_out) const {
+    const int64_t slot = h & 0xFFFFFFFFll;
+    const uint32_t gen = (uint32_t)((uint64_t)h >> 32);
+    if (h < 0 || slot >= (int64_t)slots.size()) return KV_ERR_EVICTED;
+    const StateRec& s = slots[slot];
+    if (s.status != ST_ACTIVE || s.gen != gen) return KV_ERR_EVICTED;
+    *slot_out = (int32_t)slot;
+    return KV_OK;
+  }
+  int32_t* trow(int32_t slot) const { return tables + (int64_t)slot * max_blocks; }
+};
+
+namespace {
+
+hipStream_t S(kv_stream s) { return (hipStream_t)s; }
+
+kv_status hip_ok(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_HIP; }
+
+#define KV_TRY(expr)                  \
+  do {                                \
+    kv_status _st = (expr);           \
+    if (_st != KV_OK) return _st;     \
+  } while (0)
+#define KV_HIP(expr) KV_TRY(hip_ok(expr))
+
+// Allocate on the device in request order; the caller has checked the count.
+kv_status run_alloc(kv_pool* p, const AllocArgs& a, hipStream_t s) {
+  int64_t need = 0;
+  for (int r = 0; r < a.n_req; ++r) need += a.req[r].count + (a.req[r].cow > 0);
+  if (need == 0) return KV_OK;
+  KV_HIP(launch_alloc(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P, p->head,
+                      a, p->cow, s));
+  p->head += need;
+  return KV_OK;
+}
+
+// Release states (slot, nblocks) in order; synchronous.  max_alloc < 0 releases
+// all of them.  Returns the number released.
+kv_status run_release(kv_pool* p, const std::vector<int32_t>& cand, int64_t max_alloc,
+                      hipStream_t s, int32_t* n_done) {
+  const int32_t n = (int32_t)(cand.size() / 2);
+  *n_done = 0;
+  if (n == 0) return KV_OK;
+  KV_HIP(hipMemcpyAsync(p->cmd, cand.data(), cand.size() * 4, hipMemcpyHostToDevice, s));
+  KV_HIP(launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
+                        p->cmd, n, max_alloc, p->head, p->tail, s));
+  DevHeader h;
+  KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
+  KV_HIP(hipStreamSynchronize(s));
+  if (h.status != 0 || h.head != p->head) return KV_ERR_INTERNAL;
+  p->tail = h.tail;
+  *n_done = h.n_evicted;
+  return KV_OK;
+}
+
+// Per-call launch description of an append (materialize or attend).
+AppendDesc make_desc(const kv_pool* p, const std::vector<int32_t>& slots,
+                     const std::vector<int64_t>& n_before, const std::vector<int64_t>& pos0,
+                     int64_t T) {
+  AppendDesc ad;
+  std::memset(&ad, 0, sizeof(ad));
+  ad.batch = (int32_t)slots.size();
+  ad.T = (int32_t)T;
+  int32_t max_keys = 0;
+  for (size_t i = 0; i < slots.size(); ++i) {
+    ad.seq[i].slot = slots[i];
+    ad.seq[i].n_before = (int32_t)n_before[i];
+    ad.seq[i].pos0 = (int32_t)pos0[i];
+    max_keys = std::max<int32_t>(max_keys, (int32_t)(n_before[i] + T));
+  }
+  ad.max_keys = max_keys;
+  return ad;
+}
+
+// Layers per group that fit in the scratch area (0: not even one layer).
+int layers_per_group(const kv_pool* p, const AppendDesc& ad, size_t* q_layer, size_t* extra) {
+  const kv_model_cfg& c = p->cfg;
+  const int64_t M = (int64_t)ad.batch * ad.T;
+  *q_layer = align256((size_t)M * c.n_q_heads * c.head_dim * elt_bytes(c));
+  *extra = align256(fast_scratch_bytes(p->geom(), c.dtype, ad));
+  if (p->scratch_bytes < *q_layer + *extra) return 0;
+  return (int)std::min<size_t>(c.n_layers, (p->scratch_bytes - *extra) / *q_layer);
+}
+
+// Shared path of materialize and attend: allocation (with copy-on-write),
+// projection + RoPE + paged store, and attention, layer group by layer group.
+kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, const void* x,
+                     void* o, hipStream_t s) {
+  const kv_model_cfg& c = p->cfg;
+  size_t q_layer, extra;
+  const int lc_max = layers_per_group(p, ad, &q_layer, &extra);
+  if (lc_max < 1) return KV_ERR_BUFSIZE;
+  KV_TRY(run_alloc(p, aa, s));
+  const PoolGeom g = p->geom();
+  bool any_cow = false;
+  for (int i = 0; i < aa.n_req; ++i) any_cow |= aa.req[i].cow > 0;
+  if (any_cow) KV_HIP(launch_cow(g, c.dtype, p->cow, aa, s));
+  void* part = p->scratch + q_layer * lc_max;
+  for (int l0 = 0; l0 < c.n_layers; l0 += lc_max) {
+    const int lc = std::min(lc_max, c.n_layers - l0);
+    bool done = false;
+    KV_HIP(launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s, &done));
+    if (!done)
+      KV_HIP(launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
+    done = false;
+    KV_HIP(launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done));
+    if (!done) KV_HIP(launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
+  }
+  return KV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kv_strerror(kv_status st) {
+  switch (st) {
+    case KV_OK: return "KV_OK";
+    case KV_ERR_ARG: return "KV_ERR_ARG";
+    case KV_ERR_OOM: return "KV_ERR_OOM";
+    case KV_ERR_INCOMPATIBLE: return "KV_ERR_INCOMPATIBLE";
+    case KV_ERR_EVICTED: return "KV_ERR_EVICTED";
+    case KV_ERR_BAD_HEADER: return "KV_ERR_BAD_HEADER";
+    case KV_ERR_BUFSIZE: return "KV_ERR_BUFSIZE";
+    case KV_ERR_CAPACITY: return "KV_ERR_CAPACITY";
+    case KV_ERR_HIP: return "KV_ERR_HIP";
+    case KV_ERR_INTERNAL: return "KV_ERR_INTERNAL";
+    default: return "KV_ERR_UNKNOWN";
+  }
+}
+
+kv_status kv_pool_bytes(const kv_model_cfg* cfg, int64_t n_blocks, size_t* pool_bytes,
+                        size_t* meta_bytes) {
+  KV_TRY(check_cfg(cfg));
+  if (n_blocks < 1 || n_blocks > INT32_MAX) return KV_ERR_ARG;
+  const size_t block_bytes = (size_t)cfg->n_layers * 2 * cfg->n_kv_heads * cfg->block_size *
+                             cfg->head_dim * elt_bytes(*cfg);
+  if (pool_bytes) *pool_bytes = block_bytes * n_blocks;
+  if (meta_bytes) *meta_bytes = meta_layout(*cfg, n_blocks).total;
+  return KV_OK;
+}
+
+size_t kv_scratch_bytes(const kv_model_cfg* cfg, int64_t tokens, int32_t batch,
+                        int64_t max_keys) {
+  if (check_cfg(cfg) != KV_OK || tokens < 1 || batch < 1) return 0;
+  const size_t q = (size_t)cfg->n_layers * tokens * cfg->n_q_heads * cfg->head_dim *
+                   elt_bytes(*cfg);
+  return align256(q) + fast_scratch_bound(*cfg, tokens, batch, max_keys);
+}
+
+kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_dev,
+                         void* meta_dev, void* scratch_dev, size_t scratch_bytes,
+                         const int32_t* init_free_order, kv_stream stream, kv_pool** out) {
+  KV_TRY(check_cfg(cfg));
+  if (!out || !pool_dev || !meta_dev || n_blocks < 1 || n_blocks > INT32_MAX) return KV_ERR_ARG;
+  if (((uintptr_t)pool_dev | (uintptr_t)meta_dev | (uintptr_t)scratch_dev) & 255) return KV_ERR_ARG;
+  std::vector<int32_t> order(n_blocks);
+  if (init_free_order) {
+    std::vector<char> seen(n_blocks, 0);
+    for (int64_t i = 0; i < n_blocks; ++i) {
+      const int32_t v = init_free_order[i];
+      if (v < 0 || v >= n_blocks || seen[v]) return KV_ERR_ARG;
+      seen[v] = 1;
+      order[i] = v;
+    }
+  } else {
+    for (int64_t i = 0; i < n_blocks; ++i) order[i] = (int32_t)i;
+  }
+  kv_pool* p = new (std::nothrow) kv_pool();
+  if (!p) return KV_ERR_ARG;
+  p->cfg = *cfg;
+  p->P = n_blocks;
+  p->max_blocks = (int32_t)ceil_div(cfg->max_pos, cfg->block_size);
+  p->pool = (char*)pool_dev;
+  p->meta = (char*)meta_dev;
+  p->scratch = (char*)scratch_dev;
+  p->scratch_bytes = scratch_dev ? scratch_bytes : 0;
+  p->ml = meta_layout(*cfg, n_blocks);
+  p->dhdr = (DevHeader*)(p->meta + p->ml.hdr);
+  p->rc = (int32_t*)(p->meta + p->ml.rc);
+  p->ring = (int32_t*)(p->meta + p->ml.ring);
+  p->tables = (int32_t*)(p->meta + p->ml.tables);
+  p->rope_cos = (float*)(p->meta + p->ml.rope_cos);
+  p->rope_sin = (float*)(p->meta + p->ml.rope_sin);
+  p->cow = (int2*)(p->meta + p->ml.cow);
+  p->cmd = (int32_t*)(p->meta + p->ml.cmd);
+  p->head = 0;
+  p->tail = n_blocks;
+  p->slots.resize(cfg->max_states);
+
+  // RoPE table: angle p * theta_i with theta_i = base^(-2i/dh), in double.
+  const int half = cfg->head_dim / 2;
+  std::vector<float> cs((size_t)cfg->max_pos * half), sn((size_t)cfg->max_pos * half);
+  for (int i = 0; i < half; ++i) {
+    const double th = std::pow(cfg->rope_base, -2.0 * i / cfg->head_dim);
+    for (int64_t pos = 0; pos < cfg->max_pos; ++pos) {
+      const double a = (double)pos * th;
+      cs[pos * half + i] = (float)std::cos(a);
+      sn[pos * half + i] = (float)std::sin(a);
+    }
+  }
+  DevHeader h;
+  std::memset(&h, 0, sizeof(h));
+  h.head = 0;
+  h.tail = n_blocks;
+  hipStream_t s = S(stream);
+  kv_status st = KV_OK;
+  if (hipMemsetAsync(p->meta, 0, p->ml.total, s) != hipSuccess ||
+      hipMemcpyAsync(p->dhdr, &h, sizeof(h), hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->ring, order.data(), n_blocks * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    st = KV_ERR_HIP;
+  if (st != KV_OK) {
+    delete p;
+    return st;
+  }
+  *out = p;
+  return KV_OK;
+}
+
+kv_status kv_pool_destroy(kv_pool* pool) {
+  delete pool;
+  return KV_OK;
+}
+
+kv_status kv_set_weights(kv_pool* p, const void* w_dev, int64_t layer_stride_elems) {
+  if (!p || !w_dev) return KV_ERR_ARG;
+  const int64_t per = (int64_t)(p->cfg.n_q_heads + 2 * p->cfg.n_kv_heads) * p->cfg.head_dim *
+                      p->cfg.d_model;
+  if (layer_stride_elems < per && p->cfg.n_layers > 1) return KV_ERR_ARG;
+  if ((uintptr_t)w_dev & 15) return KV_ERR_ARG;
+  p->w = w_dev;
+  p->w_stride = layer_stride_elems;
+  return KV_OK;
+}
+
+kv_status kv_materialize(kv_pool* p, const void* x_dev, int64_t T, int64_t pos0, void* o_dev,
+                         kv_stream stream, kv_state* out) {
+  if (!p || !x_dev || !o_dev || !out || T <= 0 || pos0 < 0) return KV_ERR_ARG;
+  if (!p->w) return KV_ERR_ARG;
+  const kv_model_cfg& c = p->cfg;
+  if (pos0 + T > c.max_pos) return KV_ERR_CAPACITY;
+  const int32_t slot = p->take_slot();
+  if (slot < 0) return KV_ERR_CAPACITY;
+  const int64_t nb = ceil_div(T, c.block_size);
+  if (nb > p->free_blocks()) return KV_ERR_OOM;
+  const AppendDesc ad = make_desc(p, {slot}, {0}, {pos0}, T);
+  size_t ql, ex;
+  if (layers_per_group(p, ad, &ql, &ex) < 1) return KV_ERR_BUFSIZE;
+  AllocArgs aa;
+  std::memset(&aa, 0, sizeof(aa));
+  aa.n_req = 1;
+  aa.req[0].slot = slot;
+  aa.req[0].count = (int32_t)nb;
+  StateRec& r = p->open_state(slot, pos0, T, nb,
+                              lineage_word(KV_LINEAGE_MATERIALIZE, kNoParent, 0));
+  if (T % c.block_size) r.group = p->new_group(1);
+  p->touch(r, false);
+  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
+  *out = p->handle(slot);
+  return KV_OK;
+}
+
+kv_status kv_fork(kv_pool* p, kv_state parent, int32_t k, kv_state* children, kv_stream stream) {
+  if (!p || !children || k < 1 || k > KV_MAX_FORK) return KV_ERR_ARG;
+  int32_t ps;
+  KV_TRY(p->lookup(parent, &ps));
+  if (p->live() + k > p->cfg.max_states) return KV_ERR_CAPACITY;
+  ForkArgs fa;
+  std::memset(&fa, 0, sizeof(fa));
+  fa.parent = ps;
+  fa.k = k;
+  const StateRec par = p->slots[ps];
+  fa.nblocks = (int32_t)par.nblocks;
+  std::vector<int32_t> kids;
+  for (int j = 1; j <= k; ++j) {
+    const int32_t cs = p->take_slot();
+    StateRec& c = p->open_state(cs, par.pos0, par.n, par.nblocks,
+                                lineage_word(KV_LINEAGE_FORK, (uint64_t)par.sid, j));
+    c.group = par.group;
+    fa.child[j - 1] = cs;
+    kids.push_back(cs);
+  }
+  if (par.group >= 0) p->holders[par.group] += k;
+  KV_HIP(launch_fork(p->dhdr, p->tables, p->max_blocks, p->rc, fa, S(stream)));
+  p->touch(p->slots[ps], true);
+  for (int j = 0; j < k; ++j) {
+    p->touch(p->slots[kids[j]], false);
+    children[j] = p->handle(kids[j]);
+  }
+  return KV_OK;
+}
+
+kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const void* x_dev,
+                    int64_t T, void* o_dev, kv_stream stream) {
+  if (!p || !states || !x_dev || !o_dev || batch < 1 || batch > KV_MAX_BATCH || T <= 0)
+    return KV_ERR_ARG;
+  if (!p->w) return KV_ERR_ARG;
+  for (int i = 0; i < batch; ++i)
+    for (int j = 0; j < i; ++j)
+      if (states[i] == states[j]) return KV_ERR_ARG;
+  const kv_model_cfg& c = p->cfg;
+  const int B = c.block_size;
+  std::vector<int32_t> slots(batch);
+  for (int i = 0; i < batch; ++i) KV_TRY(p->lookup(states[i], &slots[i]));
+  AllocArgs aa;
+  std::memset(&aa, 0, sizeof(aa));
+  aa.n_req = batch;
+  std::vector<int64_t> nbef(batch), pos0(batch);
+  int64_t need = 0;
+  // holders of each tail group as the batch is processed in order: a member
+  // that copies a shared tail leaves its group before the next member looks
+  std::vector<std::pair<int32_t, int32_t>> left;
+  auto holders_now = [&](int32_t g) {
+    int32_t h = p->holders[g];
+    for (const auto& e : left)
+      if (e.first == g) h -= e.second;
+    return h;
+  };
+  for (int i = 0; i < batch; ++i) {
+    const StateRec& r = p->slots[slots[i]];
+    if (r.pos0 + r.n + T > c.max_pos) return KV_ERR_CAPACITY;
+    const bool shared_tail = (r.n % B) && r.group >= 0 && holders_now(r.group) > 1;
+    if (shared_tail) left.push_back({r.group, 1});
+    aa.req[i].slot = slots[i];
+    aa.req[i].cow = shared_tail ? (int32_t)(r.n % B) : 0;
+    aa.req[i].first = (int32_t)r.nblocks;
+    aa.req[i].count = (int32_t)(ceil_div(r.n + T, B) - ceil_div(r.n, B));
+    need += aa.req[i].count + (shared_tail ? 1 : 0);
+    nbef[i] = r.n;
+    pos0[i] = r.pos0;
+  }
+  if (need > p->free_blocks()) return KV_ERR_OOM;
+  const AppendDesc ad = make_desc(p, slots, nbef, pos0, T);
+  size_t ql, ex;
+  if (layers_per_group(p, ad, &ql, &ex) < 1) return KV_ERR_BUFSIZE;
+  for (int i = 0; i < batch; ++i) {
+    StateRec& r = p->slots[slots[i]];
+    p->leave_group(r);  // after the append the tail block is private
+    r.n += T;
+    r.nblocks += aa.req[i].count;
+    if (r.n % B) r.group = p->new_group(1);
+  }
+  for (int i = 0; i < batch; ++i) p->touch(p->slots[slots[i]], true);
+  return run_append(p, ad, aa, x_dev, o_dev, S(stream));
+}
+
+kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream stream,
+                     kv_state* out) {
+  if (!p || !segs || !out || n < 1 || n > KV_MAX_SEGMENTS) return KV_ERR_ARG;
+  const kv_model_cfg& c = p->cfg;
+  const int B = c.block_size;
+  std::vector<int32_t> sl(n);
+  for (int i = 0; i < n; ++i) KV_TRY(p->lookup(segs[i].state, &sl[i]));
+  int64_t N = 0;
+  for (int i = 0; i < n; ++i) {
+    const StateRec& r = p->slots[sl[i]];
+    if (!(0 <= segs[i].tok_begin && segs[i].tok_begin < segs[i].tok_end &&
+          segs[i].tok_end <= r.n))
+      return KV_ERR_ARG;
+    N += segs[i].tok_end - segs[i].tok_begin;
+  }
+  const int64_t P0 = p->slots[sl[0]].pos0 + segs[0].tok_begin;
+  if (P0 + N > c.max_pos) return KV_ERR_CAPACITY;
+  const int32_t slot = p->take_slot();
+  if (slot < 0) return KV_ERR_CAPACITY;
+  ComposeArgs ca;
+  std::memset(&ca, 0, sizeof(ca));
+  ca.nseg = n;
+  ca.new_slot = slot;
+  ca.n_tokens = (int32_t)N;
+  ca.n_dest_blocks = (int32_t)ceil_div(N, B);
+  int64_t cum = 0, aliased = 0;
+  int32_t tail_alias_seg = -1;
+  for (int i = 0; i < n; ++i) {
+    const StateRec& r = p->slots[sl[i]];
+    const int64_t len = segs[i].tok_end - segs[i].tok_begin;
+    const int64_t off = cum - segs[i].tok_begin;
+    const int64_t delta = P0 + off - r.pos0;
+    SegDesc& sd = ca.seg[i];
+    sd.slot = sl[i];
+    sd.cum = (int32_t)cum;
+    sd.off = (int32_t)off;
+    sd.delta = (int32_t)delta;
+    sd.alias_b0 = sd.alias_b1 = 0;
+    if (delta == 0 && off % B == 0) {
+      int64_t b0 = ceil_div(cum, B), b1 = (cum + len) / B;
+      if (i == n - 1 && segs[i].tok_end == r.n && N % B && (N / B) * B >= cum) {
+        b1 += 1;  // the final partial block is the source's own tail
+        tail_alias_seg = i;
+      }
+      if (b1 > b0) {
+        sd.alias_b0 = (int32_t)b0;
+        sd.alias_b1 = (int32_t)b1;
+        aliased += b1 - b0;
+      }
+    }
+    cum += len;
+  }
+  const int64_t ncopy = ca.n_dest_blocks - aliased;
+  if (ncopy > p->free_blocks()) return KV_ERR_OOM;
+  const hipStream_t s = S(stream);
+  StateRec& r = p->open_state(slot, P0, N, ca.n_dest_blocks,
+                              lineage_word(KV_LINEAGE_MERGE, (uint64_t)p->slots[sl[0]].sid, 0));
+  KV_HIP(launch_compose_meta(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P, B,
+                             p->head, (int32_t)ncopy, ca, s));
+  p->head += ncopy;
+  if (N % B) {
+    if (tail_alias_seg >= 0 && p->slots[sl[tail_alias_seg]].group >= 0) {
+      r.group = p->slots[sl[tail_alias_seg]].group;
+      p->holders[r.group] += 1;
+    } else {
+      r.group = p->new_group(1);
+    }
+  }
+  if (ncopy > 0) KV_HIP(launch_compose_copy(p->geom(), c.dtype, ca, s));
+  for (int i = 0; i < n; ++i) p->touch(p->slots[sl[i]], true);
+  p->touch(r, false);
+  *out = p->handle(slot);
+  return KV_OK;
+}
+
+kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end, void* dst_dev,
+                  size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream) {
+  if (!p || !dst_dev || !hdr_out) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  StateRec& r = p->slots[slot];
+  if (!(0 <= blk_begin && blk_begin < blk_end && blk_end <= r.nblocks)) return KV_ERR_ARG;
+  if ((uintptr_t)dst_dev & 15) return KV_ERR_ARG;
+  const kv_model_cfg& c = p->cfg;
+  const int B = c.block_size;
+  const PoolGeom g = p->geom();
+  const uint64_t block_bytes = (uint64_t)g.block_elems * elt_bytes(c);
+  const int64_t nblk = blk_end - blk_begin;
+  if (dst_bytes < nblk * block_bytes) return KV_ERR_BUFSIZE;
+  kv_pack_header h;
+  std::memset(&h, 0, sizeof(h));
+  h.magic = KV_PACK_MAGIC;
+  h.version = KV_PACK_VERSION;
+  h.model_id = c.model_id;
+  h.cfg = c;
+  h.pos_begin = r.pos0 + blk_begin * B;
+  h.n_tokens = std::min<int64_t>(r.n, blk_end * B) - blk_begin * B;
+  h.blk_begin = blk_begin;
+  h.n_blocks = nblk;
+  h.block_bytes = block_bytes;
+  h.payload_bytes = nblk * block_bytes;
+  h.lineage = r.lineage;
+  h.src_state_id = r.sid;
+  const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * B);
+  KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid, dst_dev,
+                     S(stream)));
+  p->touch(r, true);
+  *hdr_out = h;
+  return KV_OK;
+}
+
+kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, size_t src_bytes,
+                    kv_stream stream, kv_state* out) {
+  if (!p || !hdr || !src_dev || !out) return KV_ERR_ARG;
+  if ((uintptr_t)src_dev & 15) return KV_ERR_ARG;
+  if (hdr->magic != KV_PACK_MAGIC || hdr->version != KV_PACK_VERSION) return KV_ERR_BAD_HEADER;
+  const kv_model_cfg& c = p->cfg;
+  if (hdr->model_id != c.model_id || !same_theta(hdr->cfg, c)) return KV_ERR_INCOMPATIBLE;
+  const int B = c.block_size;
+  const PoolGeom g = p->geom();
+  const uint64_t block_bytes = (uint64_t)g.block_elems * elt_bytes(c);
+  const int64_t nb = hdr->n_blocks, nt = hdr->n_tokens;
+  if (nb < 1 || !((nb - 1) * B < nt && nt <= nb * B) || hdr->block_bytes != block_bytes ||
+      hdr->payload_bytes != nb * block_bytes || hdr->pos_begin < 0)
+    return KV_ERR_BAD_HEADER;
+  if (src_bytes < hdr->payload_bytes) return KV_ERR_BUFSIZE;
+  if (hdr->pos_begin + nt > c.max_pos) return KV_ERR_CAPACITY;
+  const int32_t slot = p->take_slot();
+  if (slot < 0) return KV_ERR_CAPACITY;
+  if (nb > p->free_blocks()) return KV_ERR_OOM;
+  StateRec& r = p->open_state(slot, hdr->pos_begin, nt, nb,
+                              lineage_word(KV_LINEAGE_TRANSFER, (uint64_t)hdr->src_state_id, 0));
+  const hipStream_t s = S(stream);
+  AllocArgs aa;
+  std::memset(&aa, 0, sizeof(aa));
+  aa.n_req = 1;
+  aa.req[0].slot = slot;
+  aa.req[0].first = 0;
+  aa.req[0].count = (int32_t)nb;
+  KV_TRY(run_alloc(p, aa, s));
+  if (nt % B) r.group = p->new_group(1);
+  KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_dev, s));
+  p->touch(r, false);
+  *out = p->handle(slot);
+  return KV_OK;
+}
+
+kv_status kv_release(kv_pool* p, kv_state state, kv_stream stream) {
+  if (!p) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  StateRec& r = p->slots[slot];
+  std::vector<int32_t> cand = {slot, (int32_t)r.nblocks};
+  int32_t n = 0;
+  KV_TRY(run_release(p, cand, -1, S(stream), &n));
+  p->leave_group(r);
+  r.status = ST_RELEASED;
+  return KV_OK;
+}
+
+kv_status kv_pin(kv_pool* p, kv_state state, int32_t pinned) {
+  if (!p) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  p->slots[slot].pinned = pinned != 0;
+  return KV_OK;
+}
+
+kv_status kv_evict(kv_pool* p, int64_t max_allocated_blocks, double alpha, double beta,
+                   double gamma, kv_stream stream, int32_t* n_evicted) {
+  if (!p || !n_evicted || max_allocated_blocks < 0) return KV_ERR_ARG;
+  *n_evicted = 0;
+  struct Cand {
+    double score;
+    int64_t sid;
+    int32_t slot;
+  };
+  std::vector<Cand> cs;
+  for (size_t i = 0; i < p->slots.size(); ++i) {
+    const StateRec& r = p->slots[i];
+    if (r.status != ST_ACTIVE || r.pinned) continue;
+    const double age = (double)(p->clock - r.last_access);
+    const double score = (alpha * (double)r.reuse - beta * (double)r.nblocks) - gamma * age;
+    cs.push_back({score, r.sid, (int32_t)i});
+  }
+  std::sort(cs.begin(), cs.end(), [](const Cand& a, const Cand& b) {
+    return a.score < b.score || (a.score == b.score && a.sid < b.sid);
+  });
+  std::vector<int32_t> cand;
+  for (const auto& c : cs) {
+    cand.push_back(c.slot);
+    cand.push_back((int32_t)p->slots[c.slot].nblocks);
+  }
+  int32_t n = 0;
+  KV_TRY(run_release(p, cand, max_allocated_blocks, S(stream), &n));
+  for (int i = 0; i < n; ++i) {
+    StateRec& r = p->slots[cs[i].slot];
+    p->leave_group(r);
+    r.status = ST_EVICTED;
+  }
+  *n_evicted = n;
+  return KV_OK;
+}
+
+kv_status kv_sync(kv_pool* p, kv_stream stream) {
+  if (!p) return KV_ERR_ARG;
+  const hipStream_t s = S(stream);
+  DevHeader h;
+  KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
+  KV_HIP(hipStreamSynchronize(s));
+  if (h.status != 0) {
+    const int32_t zero = 0;
+    KV_HIP(hipMemcpyAsync(&p->dhdr->status, &zero, 4, hipMemcpyHostToDevice, s));
+    KV_HIP(hipStreamSynchronize(s));
+    return h.status;
+  }
+  if (h.head != p->head || h.tail != p->tail) return KV_ERR_INTERNAL;
+  return KV_OK;
+}
+
+kv_status kv_state_info(kv_pool* p, kv_state state, int64_t* pos0, int64_t* n_tokens,
+                        int64_t* n_blocks, uint64_t* lineage, int64_t* state_id) {
+  if (!p) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  const StateRec& r = p->slots[slot];
+  if (pos0) *pos0 = r.pos0;
+  if (n_tokens) *n_tokens = r.n;
+  if (n_blocks) *n_blocks = r.nblocks;
+  if (lineage) *lineage = r.lineage;
+  if (state_id) *state_id = r.sid;
+  return KV_OK;
+}
+
+kv_status kv_pool_counts(kv_pool* p, int64_t* free_blocks, int64_t* live_states,
+                         int64_t* clock) {
+  if (!p) return KV_ERR_ARG;
+  if (free_blocks) *free_blocks = p->free_blocks();
+  if (live_states) *live_states = p->live();
+  if (clock) *clock = p->clock;
+  return KV_OK;
+}
+
+kv_status kv_read_block_table(kv_pool* p, kv_state state, int32_t* host_out, int64_t cap,
+                              kv_stream stream) {
+  if (!p || !host_out) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  const StateRec& r = p->slots[slot];
+  if (cap < r.nblocks) return KV_ERR_BUFSIZE;
+  const hipStream_t s = S(stream);
+  KV_HIP(hipMemcpyAsync(host_out, p->trow(slot), r.nblocks * 4, hipMemcpyDeviceToHost, s));
+  KV_HIP(hipStreamSynchronize(s));
+  return KV_OK;
+}
+
+kv_status kv_read_allocator(kv_pool* p, int32_t* refcount_out, int32_t* ring_out, int64_t* head,
+                            int64_t* tail, kv_stream stream) {
+  if (!p) return KV_ERR_ARG;
+  const hipStream_t s = S(stream);
+  DevHeader h;
+  if (refcount_out)
+    KV_HIP(hipMemcpyAsync(refcount_out, p->rc, p->P * 4, hipMemcpyDeviceToHost, s));
+  if (ring_out) KV_HIP(hipMemcpyAsync(ring_out, p->ring, p->P * 4, hipMemcpyDeviceToHost, s));
+  KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
+  KV_HIP(hipStreamSynchronize(s));
+  if (head) *head = h.head;
+  if (tail) *tail = h.tail;
+  return KV_OK;
+}
+
+}  // extern "C"

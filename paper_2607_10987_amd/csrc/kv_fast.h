@@ -1,0 +1,23 @@
+// MFMA (bf16) append path: projection GEMM with fused RoPE and paged store,
+// causal prefill attention, and split-K decode attention.  Each launcher sets
+// *done = false (and enqueues nothing) when the shape is not covered, in which
+// case the portable kernels of kv_generic.hip run instead.
+#pragma once
+
+#include "kv_internal.h"
+
+namespace kvs {
+
+// Scratch bytes the fast attention needs beyond the Q buffer for this call.
+size_t fast_scratch_bytes(const PoolGeom& g, int dtype, const AppendDesc& a);
+// An upper bound of the same for calls of `tokens` new tokens over at most
+// `max_keys` keys per state.
+size_t fast_scratch_bound(const kv_model_cfg& c, int64_t tokens, int32_t batch, int64_t max_keys);
+
+hipError_t launch_qkv_fast(const PoolGeom& g, int dtype, const void* x, const void* w,
+                           int64_t w_stride, const AppendDesc& a, void* qbuf, int l0, int lc,
+                           hipStream_t s, bool* done);
+hipError_t launch_attn_fast(const PoolGeom& g, int dtype, const void* qbuf, const AppendDesc& a,
+                            void* o, void* part, int l0, int lc, hipStream_t s, bool* done);
+
+}  // namespace kvs

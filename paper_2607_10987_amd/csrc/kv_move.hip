@@ -1,0 +1,248 @@
+// Data-movement kernels over paged blocks: pack (gather a block range into a
+// contiguous transfer buffer), unpack (scatter a buffer into freshly allocated
+// blocks), copy-on-write of a shared partial tail block, and the token-granular
+// gather of compose with RoPE re-rotation of keys.
+//
+// All of them are HBM-bound streams.  One workgroup moves one (block, layer)
+// slab of 2 * Hkv * B * dh elements (64 KiB for an 8B-shaped bf16 block with
+// B = 16), using 16-byte vector accesses and several independent loads in
+// flight per thread; destination stores are non-temporal (written once, read
+// by another kernel much later).
+#include "kv_internal.h"
+
+namespace kvs {
+
+namespace {
+
+constexpr int kMoveThreads = 256;
+constexpr int kUnroll = 8;
+
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ inline void st_nt(uint4* p, const uint4& v) {
+  __builtin_nontemporal_store(v.x, &p->x);
+  __builtin_nontemporal_store(v.y, &p->y);
+  __builtin_nontemporal_store(v.z, &p->z);
+  __builtin_nontemporal_store(v.w, &p->w);
+}
+
+// Copy n16 16-byte chunks; chunk c belongs to slot (c / row16) % B and is
+// replaced by zeros when that slot is >= valid.
+__device__ inline void copy_slab(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                 int n16, int row16, int B, int valid) {
+  const int stride = kMoveThreads * kUnroll;
+  for (int base = threadIdx.x; base < n16; base += stride) {
+    uint4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int c = base + u * kMoveThreads;
+      if (c < n16) {
+        if (valid >= B || (c / row16) % B < valid) v[u] = src[c];
+        else v[u] = make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int c = base + u * kMoveThreads;
+      if (c < n16) st_nt(dst + c, v[u]);
+    }
+  }
+}
+
+// grid (nblk, L): buffer block i, layer l  <-  pool block trow[b0 + i], layer l
+__global__ void __launch_bounds__(kMoveThreads)
+k_pack(PoolGeom g, int elt, const int32_t* trow, int64_t b0, int32_t nblk, int32_t last_valid,
+       char* dst) {
+  const int i = blockIdx.x, l = blockIdx.y;
+  const int64_t block_bytes = g.block_elems * elt;
+  const int64_t layer_bytes = block_bytes / g.L;
+  const int32_t id = trow[b0 + i];
+  const char* s = (const char*)g.pool + id * block_bytes + l * layer_bytes;
+  char* d = dst + i * block_bytes + l * layer_bytes;
+  const int valid = (i == nblk - 1) ? last_valid : g.B;
+  copy_slab((const uint4*)s, (uint4*)d, (int)(layer_bytes / 16), g.dh * elt / 16, g.B, valid);
+}
+
+// grid (nblk, L): pool block trow[i], layer l  <-  buffer block i, layer l
+__global__ void __launch_bounds__(kMoveThreads)
+k_unpack(PoolGeom g, int elt, const int32_t* trow, const char* src) {
+  const int i = blockIdx.x, l = blockIdx.y;
+  const int64_t block_bytes = g.block_elems * elt;
+  const int64_t layer_bytes = block_bytes / g.L;
+  const int32_t id = trow[i];
+  const char* s = src + i * block_bytes + l * layer_bytes;
+  char* d = (char*)g.pool + id * block_bytes + l * layer_bytes;
+  copy_slab((const uint4*)s, (uint4*)d, (int)(layer_bytes / 16), g.dh * elt / 16, g.B, g.B);
+}
+
+// grid (n_req, L): for requests with cow > 0, copy slots [0, cow) of every
+// (K|V, head) tile of layer l from the old tail block to its replacement.
+__global__ void __launch_bounds__(kMoveThreads)
+k_cow(PoolGeom g, int elt, const int2* pairs, AllocArgs a) {
+  const int r = blockIdx.x, l = blockIdx.y;
+  const int m = a.req[r].cow;
+  if (m <= 0) return;
+  const int2 p = pairs[r];
+  const int64_t block_bytes = g.block_elems * elt;
+  const int tile_bytes = g.B * g.dh * elt;
+  const int run16 = m * g.dh * elt / 16;  // valid slots are a prefix of each tile
+  const int ntiles = 2 * g.Hkv;
+  const char* sb = (const char*)g.pool + p.x * block_bytes;
+  char* db = (char*)g.pool + p.y * block_bytes;
+  for (int t = 0; t < ntiles; ++t) {
+    const int64_t off = tile_off(g, l, t / g.Hkv, t % g.Hkv, 0) * elt;
+    const uint4* s = (const uint4*)(sb + off);
+    uint4* d = (uint4*)(db + off);
+    for (int c = threadIdx.x; c < run16; c += kMoveThreads) d[c] = s[c];
+  }
+  (void)tile_bytes;
+}
+
+template <typename T>
+struct Vec;
+template <>
+struct Vec<uint16_t> {  // bf16 bits: 8 per 16 bytes
+  static constexpr int N = 8;
+  __device__ static float get(const uint4& v, int i) {
+    const uint32_t w = (&v.x)[i >> 1];
+    return bf16_to_f32((uint16_t)((i & 1) ? (w >> 16) : (w & 0xffffu)));
+  }
+  __device__ static void set(uint4& v, int i, float f) {
+    uint32_t& w = (&v.x)[i >> 1];
+    const uint32_t b = f32_to_bf16(f);
+    w = (i & 1) ? ((w & 0xffffu) | (b << 16)) : ((w & 0xffff0000u) | b);
+  }
+};
+template <>
+struct Vec<float> {  // 4 per 16 bytes
+  static constexpr int N = 4;
+  __device__ static float get(const uint4& v, int i) { return __uint_as_float((&v.x)[i]); }
+  __device__ static void set(uint4& v, int i, float f) { (&v.x)[i] = __float_as_uint(f); }
+};
+
+// grid (n_dest_blocks, L).  Destination block b of the new state takes token
+// u = b*B + r from segment i (source token u - off_i).  Keys are rotated by
+// the segment's shift delta: pair (x_i, x_{i+dh/2}) -> (x cos - y sin,
+// x sin + y cos) with cos/sin of |delta| * theta_i from the float table
+// (sin negated for a negative shift).  Values and unshifted keys are copied.
+template <typename T>
+__global__ void __launch_bounds__(kMoveThreads)
+k_compose_copy(PoolGeom g, ComposeArgs a) {
+  constexpr int V = Vec<T>::N;
+  __shared__ int32_t s_src[64], s_slot[64], s_delta[64];
+  __shared__ int32_t s_dst;
+  const int b = blockIdx.x, l = blockIdx.y;
+  for (int i = 0; i < a.nseg; ++i)
+    if (b >= a.seg[i].alias_b0 && b < a.seg[i].alias_b1) return;  // aliased, nothing to copy
+  if (threadIdx.x < g.B) {
+    const int r = threadIdx.x;
+    const int u = b * g.B + r;
+    int32_t src = -1, slot = 0, delta = 0;
+    if (u < a.n_tokens) {
+      int i = 0;
+      while (i + 1 < a.nseg && a.seg[i + 1].cum <= u) ++i;
+      const int j = u - a.seg[i].off;
+      src = g.tables[(int64_t)a.seg[i].slot * g.max_blocks + j / g.B];
+      slot = j % g.B;
+      delta = a.seg[i].delta;
+    }
+    s_src[r] = src;
+    s_slot[r] = slot;
+    s_delta[r] = delta;
+  }
+  if (threadIdx.x == 0) s_dst = g.tables[(int64_t)a.new_slot * g.max_blocks + b];
+  __syncthreads();
+  T* pool = (T*)g.pool;
+  T* dblk = pool + (int64_t)s_dst * g.block_elems;
+  const int half = g.dh / 2;
+  // keys: items (head, row, chunk) over the first half of each row
+  const int kc = half / V;
+  const int nk = g.Hkv * g.B * kc;
+  for (int it = threadIdx.x; it < nk; it += kMoveThreads) {
+    const int c = it % kc;
+    const int r = (it / kc) % g.B;
+    const int h = it / (kc * g.B);
+    const int32_t src = s_src[r];
+    if (src < 0) continue;
+    const T* sp = pool + (int64_t)src * g.block_elems + tile_off(g, l, 0, h, s_slot[r]) + c * V;
+    T* dp = dblk + tile_off(g, l, 0, h, r) + c * V;
+    uint4 x = *(const uint4*)sp;
+    uint4 y = *(const uint4*)(sp + half);
+    const int delta = s_delta[r];
+    if (delta != 0) {
+      const int ad = delta < 0 ? -delta : delta;
+      const float sg = delta < 0 ? -1.f : 1.f;
+      const float* cr = g.rope_cos + (int64_t)ad * half + c * V;
+      const float* sr = g.rope_sin + (int64_t)ad * half + c * V;
+      uint4 xo = x, yo = y;
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const float cs = cr[e], sn = sg * sr[e];
+        const float xv = Vec<T>::get(x, e), yv = Vec<T>::get(y, e);
+        Vec<T>::set(xo, e, xv * cs - yv * sn);
+        Vec<T>::set(yo, e, xv * sn + yv * cs);
+      }
+      x = xo;
+      y = yo;
+    }
+    st_nt((uint4*)dp, x);
+    st_nt((uint4*)(dp + half), y);
+  }
+  // values: items (head, row, chunk) over the whole row
+  const int vc = g.dh / V;
+  const int nv = g.Hkv * g.B * vc;
+  for (int it = threadIdx.x; it < nv; it += kMoveThreads) {
+    const int c = it % vc;
+    const int r = (it / vc) % g.B;
+    const int h = it / (vc * g.B);
+    const int32_t src = s_src[r];
+    if (src < 0) continue;
+    const T* sp = pool + (int64_t)src * g.block_elems + tile_off(g, l, 1, h, s_slot[r]) + c * V;
+    T* dp = dblk + tile_off(g, l, 1, h, r) + c * V;
+    st_nt((uint4*)dp, *(const uint4*)sp);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pack(const PoolGeom& g, int dtype, const int32_t* trow, int64_t b0,
+                       int32_t nblk, int32_t last_valid, void* dst, hipStream_t s) {
+  const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
+  k_pack<<<dim3(nblk, g.L), kMoveThreads, 0, s>>>(g, elt, trow, b0, nblk, last_valid,
+                                                  (char*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const PoolGeom& g, int dtype, const int32_t* trow, int32_t nblk,
+                         const void* src, hipStream_t s) {
+  const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
+  k_unpack<<<dim3(nblk, g.L), kMoveThreads, 0, s>>>(g, elt, trow, (const char*)src);
+  return hipGetLastError();
+}
+
+hipError_t launch_cow(const PoolGeom& g, int dtype, const int2* cow_pairs, const AllocArgs& a,
+                      hipStream_t s) {
+  const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
+  k_cow<<<dim3(a.n_req, g.L), kMoveThreads, 0, s>>>(g, elt, cow_pairs, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_compose_copy(const PoolGeom& g, int dtype, const ComposeArgs& a,
+                               hipStream_t s) {
+  if (a.n_dest_blocks <= 0) return hipSuccess;
+  dim3 grid(a.n_dest_blocks, g.L);
+  if (dtype == KV_DTYPE_BF16)
+    k_compose_copy<uint16_t><<<grid, kMoveThreads, 0, s>>>(g, a);
+  else
+    k_compose_copy<float><<<grid, kMoveThreads, 0, s>>>(g, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvs

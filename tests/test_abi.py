@@ -1,0 +1,47 @@
+"""The C-ABI library loads and exports every function the header declares.
+
+CPU only: no compute call is made (there is no GPU here).
+"""
+import ctypes
+import os
+
+from paper_2607_10987_amd import kvstate as kv
+
+
+def test_library_exports_header_symbols():
+    lib = kv.lib()
+    names = kv.header_functions()
+    assert len(names) >= 20
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_covers_header():
+    for n in kv.header_functions():
+        assert callable(getattr(kv, n)), n
+
+
+def test_struct_layouts_match_header():
+    # kv_model_cfg: 10 int32 + double + uint64
+    assert ctypes.sizeof(kv.kv_model_cfg) == 56
+    assert ctypes.sizeof(kv.kv_segment) == 24
+    assert ctypes.sizeof(kv.kv_pack_header) == 8 + 8 + 56 + 4 * 8 + 3 * 8 + 8
+
+
+def test_host_only_calls():
+    c = kv.make_cfg(32, 4096, 32, 8, 128, 16, "bf16", 35072, 64)
+    pool_b, meta_b = kv.kv_pool_bytes(c, 4096)
+    assert pool_b == 4096 * 32 * 2 * 8 * 16 * 128 * 2
+    assert meta_b > 4096 * 8
+    assert kv.kv_scratch_bytes(c, 8192, 1, 8192) >= 32 * 8192 * 4096 * 2
+    assert kv.kv_strerror(kv.KV_ERR_OOM) == "KV_ERR_OOM"
+    bad = kv.make_cfg(32, 4096, 30, 8, 128, 16, "bf16", 1024, 4)   # Hq not a multiple of Hkv
+    try:
+        kv.kv_pool_bytes(bad, 16)
+        raise AssertionError("accepted a bad configuration")
+    except kv.KVError as e:
+        assert e.status == kv.KV_ERR_ARG
+
+
+def test_library_path_in_tree():
+    assert os.path.dirname(kv.LIB_PATH).endswith("paper_2607_10987_amd")

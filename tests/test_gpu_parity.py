@@ -1,0 +1,186 @@
+"""Device library vs the float64 oracle, on the GPU, through the C ABI.
+
+Every step compares block tables, refcounts and the free ring bit-exactly and
+attention outputs / pool contents within the stated tolerances (see twin.py).
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import OracleError, Status
+from paper_2607_10987_amd import kvstate as kv
+from twin import Twin, close, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def small_shape(dtype="f32", B=2, dh=16, L=1, d=32, hq=2, hkv=1):
+    return synth.ModelShape("small", L, d, hq, hkv, dh, B, dtype)
+
+
+def test_tiny_workload(gpu_available):
+    """The 256-token / 2-agent / compose / 8-decode workload, float32, in full."""
+    wl = synth.WORKLOADS["tiny"]
+    tw = Twin(wl.shape, n_blocks=64, max_pos=512, wl="tiny")
+    root = tw.materialize(wl.context)
+    a1, a2 = tw.fork(root, wl.agents)
+    tw.attend([a1, a2], wl.suffix)
+    # [shared 0..255 | agent 1 256..287 | agent 2 256..287 shifted by +32]
+    c = tw.compose([(root, 0, 256), (a1, 256, 288), (a2, 256, 288)])
+    for _ in range(wl.decode):
+        tw.attend([c], 1)
+    n = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
+    hdr, ohdr, buf, pay = tw.pack(c, 0, n)
+    u = tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.attend([u, a1], 3)
+    tw.close()
+
+
+def test_allocator_hand_trace_on_device(gpu_available):
+    tw = Twin(small_shape(), n_blocks=8, max_pos=64, wl="trace")
+    s0 = tw.materialize(5)
+    s1, s2 = tw.fork(s0, 2)
+    tw.attend([s1], 1)
+    tw.attend([s2, s0], 2)
+    tw.release(s1)
+    s3 = tw.compose([(s2, 0, 5), (s0, 4, 7)])
+    assert kv.kv_read_block_table(tw.gpu.h, s3) == [0, 1, 7, 3]
+    assert tw.evict(5) == 2
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_fork(tw.gpu.h, s2, 1)
+    assert e.value.status == kv.KV_ERR_EVICTED
+    tw.close()
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_random_sequences_on_device(gpu_available, seed):
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(40)
+    tw = Twin(small_shape(B=4), n_blocks=40, max_pos=96, max_states=10, seed=seed,
+              wl="random", order=order)
+    handles = []
+    for step in range(40):
+        live = [h for h in handles if tw.orc.states[tw.sid[h]].status == "ACTIVE"]
+        op = int(rng.integers(0, 7)) if live else 0
+        try:
+            if op == 0:
+                handles.append(tw.materialize(int(rng.integers(1, 12)),
+                                              pos0=int(rng.integers(0, 20))))
+            elif op == 1:
+                handles += tw.fork(live[rng.integers(len(live))], int(rng.integers(1, 3)))
+            elif op == 2:
+                k = int(rng.integers(1, min(3, len(live)) + 1))
+                pick = list(rng.choice(len(live), k, replace=False))
+                tw.attend([live[i] for i in pick], int(rng.integers(1, 7)))
+            elif op == 3:
+                segs = []
+                for _ in range(int(rng.integers(1, 4))):
+                    h = live[rng.integers(len(live))]
+                    n = kv.kv_state_info(tw.gpu.h, h)["n_tokens"]
+                    a = int(rng.integers(0, n))
+                    segs.append((h, a, int(rng.integers(a + 1, n + 1))))
+                handles.append(tw.compose(segs))
+            elif op == 4:
+                h = live[rng.integers(len(live))]
+                nb = kv.kv_state_info(tw.gpu.h, h)["n_blocks"]
+                b0 = int(rng.integers(0, nb))
+                hdr, ohdr, buf, pay = tw.pack(h, b0, nb)
+                handles.append(tw.unpack(hdr, ohdr, buf, pay, rerotated=h in tw.rerot))
+            elif op == 5:
+                tw.evict(int(rng.integers(0, 40)))
+            else:
+                tw.release(live[rng.integers(len(live))])
+        except kv.KVError as e:
+            # the oracle must refuse the same call with the same status; its
+            # state is unchanged, so the device tables must still match
+            assert e.status in (kv.KV_ERR_OOM, kv.KV_ERR_CAPACITY), e
+            tw.check_meta()
+    tw.close()
+
+
+def test_bf16_llama_shape_two_layers(gpu_available):
+    """8B-shaped heads (32 q / 8 kv, dh 128, B 16), 2 layers, ragged lengths."""
+    shape = synth.LLAMA8B_SHAPE
+    shape = synth.ModelShape("8b-l2", 2, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
+                             shape.head_dim, shape.block_size, "bf16")
+    tw = Twin(shape, n_blocks=160, max_pos=2048, wl="mid")
+    root = tw.materialize(1000)                    # 1000 mod 16 = 8: partial tail
+    kids = tw.fork(root, 3)
+    tw.attend(kids, 100)                           # copy-on-write of the shared tail
+    for _ in range(3):
+        tw.attend(kids, 1)                         # batched decode
+    c = tw.compose([(root, 0, 1000), (kids[0], 1000, 1100), (kids[1], 1000, 1100)])
+    tw.attend([c], 1)
+    hdr, ohdr, buf, pay = tw.pack(c, 2, 40)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.close()
+
+
+def test_pack_unpack_bit_exact_round_trips(gpu_available):
+    for dtype in ("f32", "bf16"):
+        shape = small_shape(dtype, B=4, dh=32, L=3, hq=4, hkv=2)
+        order = np.random.default_rng(5).permutation(32)
+        tw = Twin(shape, n_blocks=32, max_pos=128, wl="rt" + dtype, order=order)
+        # a seeded payload: both sides hold identical stored values
+        hdr, ohdr, buf, pay = tw.synthetic_transfer(5, 18, 7, tag=1)
+        u = tw.unpack(hdr, ohdr, buf, pay)
+        hdr2, ohdr2, buf2, pay2 = tw.pack(u, 0, 5)
+        # device bytes equal the oracle's values exactly (zero-filled tail slots)
+        got = to_np(buf2.view(tw.tdt)).reshape(pay2.shape)
+        assert np.array_equal(got, pay2)
+        # device pack o unpack o pack is the identity on bytes, through a permuted pool
+        v = kv.kv_unpack(tw.gpu.h, hdr2, buf2)
+        buf3 = torch.empty_like(buf2)
+        kv.kv_pack(tw.gpu.h, v, 0, 5, buf3)
+        torch.cuda.synchronize()
+        assert torch.equal(buf3, buf2)
+        tw.close()
+
+
+def test_error_codes_on_device(gpu_available):
+    tw = Twin(small_shape(B=2), n_blocks=4, max_pos=16, max_states=3, wl="err")
+    x = torch.zeros((9, 32), dtype=torch.float32, device="cuda")
+    o = torch.zeros((1, 9, 32), dtype=torch.float32, device="cuda")
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_materialize(tw.gpu.h, x, 9, 0, o)
+    assert e.value.status == kv.KV_ERR_OOM
+    assert kv.kv_pool_counts(tw.gpu.h)["free_blocks"] == 4
+    s = tw.materialize(4)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_attend(tw.gpu.h, [s], x, 13, o)
+    assert e.value.status == kv.KV_ERR_CAPACITY
+    for k, code in ((0, kv.KV_ERR_ARG), (3, kv.KV_ERR_CAPACITY)):
+        with pytest.raises(kv.KVError) as e:
+            kv.kv_fork(tw.gpu.h, s, k)
+        assert e.value.status == code
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_attend(tw.gpu.h, [s, s], x, 1, o)
+    assert e.value.status == kv.KV_ERR_ARG
+    buf = torch.empty(2 * tw.s.block_bytes, dtype=torch.uint8, device="cuda")
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pack(tw.gpu.h, s, 0, 2, buf, dst_bytes=2 * tw.s.block_bytes - 1)
+    assert e.value.status == kv.KV_ERR_BUFSIZE
+    hdr = kv.kv_pack(tw.gpu.h, s, 0, 2, buf)
+    for field, val, code in (("magic", 1, kv.KV_ERR_BAD_HEADER),
+                             ("model_id", 99, kv.KV_ERR_INCOMPATIBLE),
+                             ("n_tokens", 5, kv.KV_ERR_BAD_HEADER)):
+        h2 = kv.kv_pack_header.from_buffer_copy(hdr)
+        setattr(h2, field, val)
+        with pytest.raises(kv.KVError) as e:
+            kv.kv_unpack(tw.gpu.h, h2, buf)
+        assert e.value.status == code
+    h2 = kv.kv_pack_header.from_buffer_copy(hdr)
+    h2.cfg.block_size = 4
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_unpack(tw.gpu.h, h2, buf)
+    assert e.value.status == kv.KV_ERR_INCOMPATIBLE
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_unpack(tw.gpu.h, hdr, buf, src_bytes=hdr.payload_bytes - 1)
+    assert e.value.status == kv.KV_ERR_BUFSIZE
+    kv.kv_release(tw.gpu.h, s)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pack(tw.gpu.h, s, 0, 1, buf)
+    assert e.value.status == kv.KV_ERR_EVICTED
+    kv.kv_sync(tw.gpu.h)
+    tw.close()
