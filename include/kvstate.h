@@ -211,6 +211,33 @@ kv_status kv_read_block_table(kv_pool* pool, kv_state state, int32_t* host_out, 
 kv_status kv_read_allocator(kv_pool* pool, int32_t* refcount_out, int32_t* ring_out,
                             int64_t* head, int64_t* tail, kv_stream stream);
 
+/* Per-kernel timing.  While enabled, every kernel the pool launches is
+ * bracketed by HIP events recorded on its launch stream; kv_profile_read
+ * waits for them and returns, per kernel kind, the number of launches and
+ * their summed duration since the last read (then clears the counters). */
+enum {
+  KV_KERNEL_ALLOC = 0,
+  KV_KERNEL_FORK,
+  KV_KERNEL_RELEASE,
+  KV_KERNEL_COMPOSE_META,
+  KV_KERNEL_COMPOSE_COPY,
+  KV_KERNEL_PACK,
+  KV_KERNEL_UNPACK,
+  KV_KERNEL_COW,
+  KV_KERNEL_QKV,         /* projection + RoPE + paged store, T > 1 */
+  KV_KERNEL_QKV_DECODE,  /* the same for T = 1 */
+  KV_KERNEL_ATTN,        /* causal attention, T > 1 */
+  KV_KERNEL_ATTN_DECODE, /* attention for T = 1 (split-key partials) */
+  KV_KERNEL_MERGE,       /* merge of split-key partials */
+  KV_KERNEL_KINDS
+};
+typedef struct {
+  int64_t launches;
+  double total_ms;
+} kv_profile_entry;
+kv_status kv_profile_enable(kv_pool* pool, int32_t enabled);
+kv_status kv_profile_read(kv_pool* pool, kv_profile_entry* out /* KV_KERNEL_KINDS */);
+
 /* Human-readable name of a status. */
 const char* kv_strerror(kv_status status);
 

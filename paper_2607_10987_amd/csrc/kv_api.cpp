@@ -119,6 +119,32 @@ struct kv_pool {
   std::vector<int32_t> free_groups;
   const void* w = nullptr;
   int64_t w_stride = 0;
+  // kernel timing (kv_profile_*)
+  bool prof = false;
+  struct Rec {
+    int kind;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> spare;
+  kv_profile_entry acc[KV_KERNEL_KINDS] = {};
+  hipEvent_t ev() {
+    hipEvent_t e = nullptr;
+    if (!spare.empty()) {
+      e = spare.back();
+      spare.pop_back();
+    } else if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+    }
+    return e;
+  }
+  ~kv_pool() {
+    for (auto& r : pending) {
+      hipEventDestroy(r.a);
+      hipEventDestroy(r.b);
+    }
+    for (auto e : spare) hipEventDestroy(e);
+  }
 
   PoolGeom geom() const {
     PoolGeom g;
@@ -212,13 +238,37 @@ kv_status hip_ok(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_HIP; }
   } while (0)
 #define KV_HIP(expr) KV_TRY(hip_ok(expr))
 
+// Brackets the kernel launches of one scope with events when profiling is on.
+struct Timed {
+  kv_pool* p;
+  int kind;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  Timed(kv_pool* p_, int kind_, hipStream_t s_) : p(p_), kind(kind_), s(s_) {
+    if (p->prof && (a = p->ev())) hipEventRecord(a, s);
+  }
+  ~Timed() {
+    if (!a) return;
+    hipEvent_t b = p->ev();
+    if (b && hipEventRecord(b, s) == hipSuccess) {
+      p->pending.push_back({kind, a, b});
+    } else {
+      p->spare.push_back(a);
+      if (b) p->spare.push_back(b);
+    }
+  }
+};
+
 // Allocate on the device in request order; the caller has checked the count.
 kv_status run_alloc(kv_pool* p, const AllocArgs& a, hipStream_t s) {
   int64_t need = 0;
   for (int r = 0; r < a.n_req; ++r) need += a.req[r].count + (a.req[r].cow > 0);
   if (need == 0) return KV_OK;
-  KV_HIP(launch_alloc(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P, p->head,
-                      a, p->cow, s));
+  {
+    Timed t(p, KV_KERNEL_ALLOC, s);
+    KV_HIP(launch_alloc(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
+                        p->head, a, p->cow, s));
+  }
   p->head += need;
   return KV_OK;
 }
@@ -231,8 +281,11 @@ kv_status run_release(kv_pool* p, const std::vector<int32_t>& cand, int64_t max_
   *n_done = 0;
   if (n == 0) return KV_OK;
   KV_HIP(hipMemcpyAsync(p->cmd, cand.data(), cand.size() * 4, hipMemcpyHostToDevice, s));
-  KV_HIP(launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
-                        p->cmd, n, max_alloc, p->head, p->tail, s));
+  {
+    Timed t(p, KV_KERNEL_RELEASE, s);
+    KV_HIP(launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
+                          p->cmd, n, max_alloc, p->head, p->tail, s));
+  }
   DevHeader h;
   KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
   KV_HIP(hipStreamSynchronize(s));
@@ -283,17 +336,32 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
   const PoolGeom g = p->geom();
   bool any_cow = false;
   for (int i = 0; i < aa.n_req; ++i) any_cow |= aa.req[i].cow > 0;
-  if (any_cow) KV_HIP(launch_cow(g, c.dtype, p->cow, aa, s));
+  if (any_cow) {
+    Timed t(p, KV_KERNEL_COW, s);
+    KV_HIP(launch_cow(g, c.dtype, p->cow, aa, s));
+  }
   void* part = p->scratch + q_layer * lc_max;
   for (int l0 = 0; l0 < c.n_layers; l0 += lc_max) {
     const int lc = std::min(lc_max, c.n_layers - l0);
     bool done = false;
-    KV_HIP(launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s, &done));
-    if (!done)
-      KV_HIP(launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
+    {
+      Timed t(p, ad.T == 1 ? KV_KERNEL_QKV_DECODE : KV_KERNEL_QKV, s);
+      KV_HIP(launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s,
+                             &done));
+      if (!done)
+        KV_HIP(launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
+    }
     done = false;
-    KV_HIP(launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done));
-    if (!done) KV_HIP(launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
+    bool merge = false;
+    {
+      Timed t(p, ad.T == 1 ? KV_KERNEL_ATTN_DECODE : KV_KERNEL_ATTN, s);
+      KV_HIP(launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done, &merge));
+      if (!done) KV_HIP(launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
+    }
+    if (merge) {
+      Timed t(p, KV_KERNEL_MERGE, s);
+      KV_HIP(launch_attn_merge(g, c.dtype, ad, o, part, l0, lc, s));
+    }
   }
   return KV_OK;
 }
@@ -473,7 +541,10 @@ kv_status kv_fork(kv_pool* p, kv_state parent, int32_t k, kv_state* children, kv
     kids.push_back(cs);
   }
   if (par.group >= 0) p->holders[par.group] += k;
-  KV_HIP(launch_fork(p->dhdr, p->tables, p->max_blocks, p->rc, fa, S(stream)));
+  {
+    Timed t(p, KV_KERNEL_FORK, S(stream));
+    KV_HIP(launch_fork(p->dhdr, p->tables, p->max_blocks, p->rc, fa, S(stream)));
+  }
   p->touch(p->slots[ps], true);
   for (int j = 0; j < k; ++j) {
     p->touch(p->slots[kids[j]], false);
@@ -593,8 +664,11 @@ kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream st
   const hipStream_t s = S(stream);
   StateRec& r = p->open_state(slot, P0, N, ca.n_dest_blocks,
                               lineage_word(KV_LINEAGE_MERGE, (uint64_t)p->slots[sl[0]].sid, 0));
-  KV_HIP(launch_compose_meta(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P, B,
-                             p->head, (int32_t)ncopy, ca, s));
+  {
+    Timed t(p, KV_KERNEL_COMPOSE_META, s);
+    KV_HIP(launch_compose_meta(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks,
+                               (int32_t)p->P, B, p->head, (int32_t)ncopy, ca, s));
+  }
   p->head += ncopy;
   if (N % B) {
     if (tail_alias_seg >= 0 && p->slots[sl[tail_alias_seg]].group >= 0) {
@@ -604,7 +678,10 @@ kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream st
       r.group = p->new_group(1);
     }
   }
-  if (ncopy > 0) KV_HIP(launch_compose_copy(p->geom(), c.dtype, ca, s));
+  if (ncopy > 0) {
+    Timed t(p, KV_KERNEL_COMPOSE_COPY, s);
+    KV_HIP(launch_compose_copy(p->geom(), c.dtype, ca, s));
+  }
   for (int i = 0; i < n; ++i) p->touch(p->slots[sl[i]], true);
   p->touch(r, false);
   *out = p->handle(slot);
@@ -640,8 +717,11 @@ kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end
   h.lineage = r.lineage;
   h.src_state_id = r.sid;
   const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * B);
-  KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid, dst_dev,
-                     S(stream)));
+  {
+    Timed t(p, KV_KERNEL_PACK, S(stream));
+    KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid, dst_dev,
+                       S(stream)));
+  }
   p->touch(r, true);
   *hdr_out = h;
   return KV_OK;
@@ -677,7 +757,10 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
   aa.req[0].count = (int32_t)nb;
   KV_TRY(run_alloc(p, aa, s));
   if (nt % B) r.group = p->new_group(1);
-  KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_dev, s));
+  {
+    Timed t(p, KV_KERNEL_UNPACK, s);
+    KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_dev, s));
+  }
   p->touch(r, false);
   *out = p->handle(slot);
   return KV_OK;
@@ -804,6 +887,31 @@ kv_status kv_read_allocator(kv_pool* p, int32_t* refcount_out, int32_t* ring_out
   KV_HIP(hipStreamSynchronize(s));
   if (head) *head = h.head;
   if (tail) *tail = h.tail;
+  return KV_OK;
+}
+
+kv_status kv_profile_enable(kv_pool* p, int32_t enabled) {
+  if (!p) return KV_ERR_ARG;
+  p->prof = enabled != 0;
+  return KV_OK;
+}
+
+kv_status kv_profile_read(kv_pool* p, kv_profile_entry* out) {
+  if (!p || !out) return KV_ERR_ARG;
+  for (auto& r : p->pending) {
+    KV_HIP(hipEventSynchronize(r.b));
+    float ms = 0.f;
+    KV_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    p->acc[r.kind].launches += 1;
+    p->acc[r.kind].total_ms += ms;
+    p->spare.push_back(r.a);
+    p->spare.push_back(r.b);
+  }
+  p->pending.clear();
+  for (int k = 0; k < KV_KERNEL_KINDS; ++k) {
+    out[k] = p->acc[k];
+    p->acc[k] = kv_profile_entry{0, 0.0};
+  }
   return KV_OK;
 }
 

@@ -17,7 +17,12 @@ size_t fast_scratch_bound(const kv_model_cfg& c, int64_t tokens, int32_t batch, 
 hipError_t launch_qkv_fast(const PoolGeom& g, int dtype, const void* x, const void* w,
                            int64_t w_stride, const AppendDesc& a, void* qbuf, int l0, int lc,
                            hipStream_t s, bool* done);
+// *merge = true when the launch wrote split-key partials that
+// launch_attn_merge must combine into o.
 hipError_t launch_attn_fast(const PoolGeom& g, int dtype, const void* qbuf, const AppendDesc& a,
-                            void* o, void* part, int l0, int lc, hipStream_t s, bool* done);
+                            void* o, void* part, int l0, int lc, hipStream_t s, bool* done,
+                            bool* merge);
+hipError_t launch_attn_merge(const PoolGeom& g, int dtype, const AppendDesc& a, void* o,
+                             const void* part, int l0, int lc, hipStream_t s);
 
 }  // namespace kvs

@@ -3,20 +3,59 @@
 
 namespace kvs {
 
-size_t fast_scratch_bytes(const PoolGeom&, int, const AppendDesc&) { return 0; }
+int decode_chunks(const AppendDesc& a);
+bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a);
+size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a);
+hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
+                              void* part, int lc, int l0, hipStream_t s);
+hipError_t launch_decode_merge(const PoolGeom& g, const AppendDesc& a, void* o, const void* part,
+                               int l0, int lc, hipStream_t s);
 
-size_t fast_scratch_bound(const kv_model_cfg&, int64_t, int32_t, int64_t) { return 0; }
-
-hipError_t launch_qkv_fast(const PoolGeom&, int, const void*, const void*, int64_t,
-                           const AppendDesc&, void*, int, int, hipStream_t, bool* done) {
-  *done = false;
-  return hipSuccess;
+size_t fast_scratch_bytes(const PoolGeom& g, int dtype, const AppendDesc& a) {
+  return decode_mfma_ok(g, dtype, a) ? decode_part_bytes(g, a) : 0;
 }
 
-hipError_t launch_attn_fast(const PoolGeom&, int, const void*, const AppendDesc&, void*, void*,
-                            int, int, hipStream_t, bool* done) {
+size_t fast_scratch_bound(const kv_model_cfg& c, int64_t, int32_t batch, int64_t max_keys) {
+  // split-key partials of a decode call: L x batch x Hq x chunks x (4 + dh) floats
+  const int64_t chunks = (max_keys + 511) / 512;
+  return (size_t)c.n_layers * batch * c.n_q_heads * chunks * (c.head_dim + 4) * sizeof(float);
+}
+
+bool qkv_mfma_ok(const PoolGeom& g, int dtype);
+hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int64_t w_stride,
+                           const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s);
+
+hipError_t launch_qkv_fast(const PoolGeom& g, int dtype, const void* x, const void* w,
+                           int64_t w_stride, const AppendDesc& a, void* qbuf, int l0, int lc,
+                           hipStream_t s, bool* done) {
   *done = false;
-  return hipSuccess;
+  if (!qkv_mfma_ok(g, dtype)) return hipSuccess;
+  *done = true;
+  return launch_qkv_mfma(g, x, w, w_stride, a, qbuf, l0, lc, s);
+}
+
+bool attn_mfma_ok(const PoolGeom& g, int dtype);
+hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const AppendDesc& a, void* o,
+                               int l0, int lc, hipStream_t s);
+
+hipError_t launch_attn_fast(const PoolGeom& g, int dtype, const void* qbuf, const AppendDesc& a,
+                            void* o, void* part, int l0, int lc, hipStream_t s, bool* done,
+                            bool* merge) {
+  *done = false;
+  *merge = false;
+  if (decode_mfma_ok(g, dtype, a)) {
+    *done = true;
+    *merge = true;
+    return launch_decode_attn(g, qbuf, a, part, lc, l0, s);
+  }
+  if (!attn_mfma_ok(g, dtype)) return hipSuccess;
+  *done = true;
+  return launch_attn_prefill(g, qbuf, a, o, l0, lc, s);
+}
+
+hipError_t launch_attn_merge(const PoolGeom& g, int, const AppendDesc& a, void* o,
+                             const void* part, int l0, int lc, hipStream_t s) {
+  return launch_decode_merge(g, a, o, part, l0, lc, s);
 }
 
 }  // namespace kvs

@@ -1,0 +1,286 @@
+// QKV projection on MFMA (bf16 in, fp32 accumulate) with the RoPE rotation
+// and the paged K/V store fused into the epilogue.
+//
+// The kernel computes C^T = W_l X^T: the A operand is a 32-row slab of the
+// weight rows (output channels), the B operand a 32-row slab of the token
+// rows, both K-contiguous, so tiles are staged through LDS with 16-byte
+// accesses and read back with one ds_read_b128 per MFMA operand.  In the
+// C^T layout of v_mfma_f32_32x32x16_bf16 a lane holds, for one token, four
+// consecutive output channels per group, so RoPE partners (channel i and
+// i + 64 of the same head) sit in the same lane when one wavefront owns a
+// whole 128-channel head, and stores are 8-byte runs of one token row.
+//
+// Two tilings:
+//   prefill  (T > 1): 256 channels (2 heads) x 256 tokens per workgroup, four
+//            waves of 128 x 128, K step 64, double-buffered LDS (144 KiB),
+//            RoPE in registers, bf16 tile restaged through LDS so that the
+//            final Q / K / V stores are 16-byte, row-contiguous writes;
+//   decode   (T = 1, at most 32 tokens): 128 channels (1 head) x 32 tokens,
+//            four waves of 32 channels, fp32 tile in LDS for the rotation.
+// Q goes to the scratch buffer [lc][M][Hq * dh]; K and V rows go to
+// pool[table[slot][u / B]][l][K|V][kv head][u % B][:] with u = n_before + t.
+#include "kv_fast.h"
+
+namespace kvs {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBK = 64;
+constexpr int kLd = kBK + 8;  // LDS row stride in elements (144 bytes)
+constexpr int kThreads = 256;
+constexpr int kDh = 128;
+
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+  const __bf16 x = (__bf16)a, y = (__bf16)b;  // round to nearest even
+  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+}
+
+// Row m of the token matrix -> destination description.
+struct RowInfo {
+  int seq, t, u, pos, slot;
+};
+
+__device__ inline RowInfo row_info(const AppendDesc& a, int row) {
+  RowInfo r;
+  r.seq = row / a.T;
+  r.t = row - r.seq * a.T;
+  const SeqDesc sd = a.seq[r.seq];
+  r.u = sd.n_before + r.t;
+  r.pos = sd.pos0 + r.u;
+  r.slot = sd.slot;
+  return r;
+}
+
+// Destination of 8 consecutive channels [c, c + 8) of layer-local head `hh`
+// (0 .. Hq + 2 Hkv - 1) for token row `row`.
+__device__ inline uint16_t* dest(const PoolGeom& g, const AppendDesc& a, uint16_t* qbuf, int lc,
+                                 int l, int M, int row, int hh, int c) {
+  if (hh < g.Hq) return qbuf + (((int64_t)lc * M + row) * g.Hq + hh) * kDh + c;
+  const RowInfo r = row_info(a, row);
+  const int kv = hh < g.Hq + g.Hkv ? 0 : 1;
+  const int gh = hh - g.Hq - kv * g.Hkv;
+  const int32_t blk = g.tables[(int64_t)r.slot * g.max_blocks + r.u / g.B];
+  return (uint16_t*)g.pool + (int64_t)blk * g.block_elems + tile_off(g, l, kv, gh, r.u % g.B) + c;
+}
+
+template <int CH, int BT, int WCH, int WTK>
+struct Tiling {
+  static constexpr int TI = CH / WCH / 32;  // channel tiles per wave
+  static constexpr int TJ = BT / WTK / 32;  // token tiles per wave
+  static constexpr int WAVE_CH = CH / WCH;
+  static constexpr int STAGE = (CH + BT) * kLd;            // elements per LDS stage
+  static constexpr int A_LD = CH * kBK / 8 / kThreads;     // 16-byte loads per thread
+  static constexpr int B_LD = (BT * kBK / 8 + kThreads - 1) / kThreads;
+  static constexpr bool WAVE_HEAD = WAVE_CH == kDh;         // wave owns a whole head
+  static constexpr int EPI_BYTES = WAVE_HEAD ? BT * (CH + 8) * 2 : BT * (CH + 4) * 4;
+  static constexpr int MAIN_BYTES = 2 * STAGE * 2;
+  static constexpr int SMEM = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+};
+
+template <int CH, int BT, int WCH, int WTK>
+__global__ void __launch_bounds__(kThreads)
+k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+           int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
+  using TL = Tiling<CH, BT, WCH, WTK>;
+  constexpr int TI = TL::TI, TJ = TL::TJ;
+  __shared__ __attribute__((aligned(16))) char smem_raw[TL::SMEM];
+  uint16_t* smem = (uint16_t*)smem_raw;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * CH;  // first output channel of the layer
+  const int m0 = blockIdx.y * BT;  // first token row
+  const int lc = blockIdx.z, l = l0 + lc;
+  const int M = a.batch * a.T, d = g.d;
+  const uint16_t* wl = w + (int64_t)l * w_stride;
+  const int ch0 = (wave % WCH) * TL::WAVE_CH;
+  const int tk0 = (wave / WCH) * (BT / WTK);
+
+  uint4 ra[TL::A_LD], rb[TL::B_LD];
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < TL::A_LD; ++i) {
+      const int q = tid + kThreads * i, r = q >> 3, c = q & 7;
+      ra[i] = *(const uint4*)(wl + (int64_t)(n0 + r) * d + kb * kBK + c * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < TL::B_LD; ++i) {
+      const int q = tid + kThreads * i, r = q >> 3, c = q & 7;
+      const int row = m0 + r;
+      rb[i] = (r < BT && row < M) ? *(const uint4*)(x + (int64_t)row * d + kb * kBK + c * 8)
+                                  : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto sstore = [&](int buf) {
+    uint16_t* As = smem + buf * TL::STAGE;
+    uint16_t* Bs = As + CH * kLd;
+#pragma unroll
+    for (int i = 0; i < TL::A_LD; ++i) {
+      const int q = tid + kThreads * i, r = q >> 3, c = q & 7;
+      *(uint4*)(As + r * kLd + c * 8) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < TL::B_LD; ++i) {
+      const int q = tid + kThreads * i, r = q >> 3, c = q & 7;
+      if (r < BT) *(uint4*)(Bs + r * kLd + c * 8) = rb[i];
+    }
+  };
+
+  floatx16 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = d / kBK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kb = 0; kb < nk; ++kb) {
+    const int cur = kb & 1;
+    if (kb + 1 < nk) gload(kb + 1);
+    const uint16_t* As = smem + cur * TL::STAGE;
+    const uint16_t* Bs = As + CH * kLd;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      bf16x8 fa[TI], fb[TJ];
+      const int kof = ks * 16 + (lane >> 5) * 8;
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+        fa[i] = *(const bf16x8*)(As + (ch0 + i * 32 + (lane & 31)) * kLd + kof);
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        fb[j] = *(const bf16x8*)(Bs + (tk0 + j * 32 + (lane & 31)) * kLd + kof);
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (kb + 1 < nk) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  const int half = kDh / 2;
+  if constexpr (TL::WAVE_HEAD) {
+    // ---- prefill epilogue: rotate in registers, restage bf16 rows in LDS
+    constexpr int SLD = CH + 8;
+    uint16_t* S = smem;
+    const int hh = (n0 + ch0) / kDh;
+    const bool rot = hh < g.Hq + g.Hkv;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int tl = tk0 + j * 32 + (lane & 31);
+      const int row = m0 + tl;
+      const int pos = row < M ? row_info(a, row).pos : 0;
+      const float* cr = g.rope_cos + (int64_t)pos * half;
+      const float* sr = g.rope_sin + (int64_t)pos * half;
+#pragma unroll
+      for (int i = 0; i < TI / 2; ++i) {
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int f0 = i * 32 + e4 * 8 + (lane >> 5) * 4;
+          float4 cs = make_float4(1.f, 1.f, 1.f, 1.f), sn = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (rot) {
+            cs = *(const float4*)(cr + f0);
+            sn = *(const float4*)(sr + f0);
+          }
+          float xr[4], yr[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float xv = acc[i][j][e4 * 4 + q], yv = acc[i + 2][j][e4 * 4 + q];
+            const float c = (&cs.x)[q], s = (&sn.x)[q];
+            xr[q] = xv * c - yv * s;
+            yr[q] = xv * s + yv * c;
+          }
+          uint2 px = make_uint2(pack_bf16x2(xr[0], xr[1]), pack_bf16x2(xr[2], xr[3]));
+          uint2 py = make_uint2(pack_bf16x2(yr[0], yr[1]), pack_bf16x2(yr[2], yr[3]));
+          *(uint2*)(S + tl * SLD + ch0 + f0) = px;
+          *(uint2*)(S + tl * SLD + ch0 + half + f0) = py;
+        }
+      }
+    }
+    __syncthreads();
+    constexpr int G8 = CH / 8;  // 16-byte groups per token row
+    for (int q = tid; q < BT * G8; q += kThreads) {
+      const int r = q / G8, c8 = q % G8;
+      const int row = m0 + r;
+      if (row >= M) continue;
+      const uint4 v = *(const uint4*)(S + r * SLD + c8 * 8);
+      const int ch = n0 + c8 * 8;
+      *(uint4*)dest(g, a, qbuf, lc, l, M, row, ch / kDh, ch % kDh) = v;
+    }
+  } else {
+    // ---- decode epilogue: fp32 tile in LDS, pairs straddle waves
+    constexpr int FLD = CH + 4;
+    float* Cf = (float*)smem_raw;
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int ch = ch0 + i * 32 + e4 * 8 + (lane >> 5) * 4;
+          const int tl = tk0 + j * 32 + (lane & 31);
+          *(float4*)(Cf + tl * FLD + ch) =
+              make_float4(acc[i][j][e4 * 4], acc[i][j][e4 * 4 + 1], acc[i][j][e4 * 4 + 2],
+                          acc[i][j][e4 * 4 + 3]);
+        }
+    __syncthreads();
+    constexpr int NH = CH / kDh;
+    for (int it = tid; it < BT * NH * (half / 4); it += kThreads) {
+      const int f4 = it % (half / 4);
+      const int hl = (it / (half / 4)) % NH;
+      const int r = it / ((half / 4) * NH);
+      const int row = m0 + r;
+      if (row >= M) continue;
+      const int hh = (n0 / kDh) + hl;
+      const float4 xv = *(const float4*)(Cf + r * FLD + hl * kDh + f4 * 4);
+      const float4 yv = *(const float4*)(Cf + r * FLD + hl * kDh + half + f4 * 4);
+      float4 xo = xv, yo = yv;
+      if (hh < g.Hq + g.Hkv) {
+        const int pos = row_info(a, row).pos;
+        const float4 cs = *(const float4*)(g.rope_cos + (int64_t)pos * half + f4 * 4);
+        const float4 sn = *(const float4*)(g.rope_sin + (int64_t)pos * half + f4 * 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float c = (&cs.x)[q], s = (&sn.x)[q];
+          (&xo.x)[q] = (&xv.x)[q] * c - (&yv.x)[q] * s;
+          (&yo.x)[q] = (&xv.x)[q] * s + (&yv.x)[q] * c;
+        }
+      }
+      uint16_t* dp = dest(g, a, qbuf, lc, l, M, row, hh, f4 * 4);
+      *(uint2*)dp = make_uint2(pack_bf16x2(xo.x, xo.y), pack_bf16x2(xo.z, xo.w));
+      *(uint2*)(dp + half) = make_uint2(pack_bf16x2(yo.x, yo.y), pack_bf16x2(yo.z, yo.w));
+    }
+  }
+}
+
+}  // namespace
+
+bool qkv_mfma_ok(const PoolGeom& g, int dtype) {
+  return dtype == KV_DTYPE_BF16 && g.dh == kDh && g.d % kBK == 0 &&
+         ((g.Hq + 2 * g.Hkv) * kDh) % 256 == 0;
+}
+
+hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int64_t w_stride,
+                           const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s) {
+  const int M = a.batch * a.T;
+  const int N = (g.Hq + 2 * g.Hkv) * kDh;
+  if (M <= 32) {
+    dim3 grid(N / 128, 1, lc);
+    k_qkv_mfma<128, 32, 4, 1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
+                                                        w_stride, a, (uint16_t*)qbuf, l0);
+  } else {
+    dim3 grid(N / 256, (M + 255) / 256, lc);
+    k_qkv_mfma<256, 256, 2, 2><<<grid, kThreads, 0, s>>>(
+        g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kvs

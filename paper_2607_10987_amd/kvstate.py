@@ -94,6 +94,8 @@ _SIGS = {
     "kv_read_block_table": (_I32, [_P, _I64, _PI32, _I64, _P]),
     "kv_read_allocator": (_I32, [_P, _PI32, _PI32, _PI64, _PI64, _P]),
     "kv_strerror": (ctypes.c_char_p, [_I32]),
+    "kv_profile_enable": (_I32, [_P, _I32]),
+    "kv_profile_read": (_I32, [_P, ctypes.c_void_p]),
 }
 
 _lib = None
@@ -287,6 +289,25 @@ def kv_read_allocator(pool, n_blocks: int, stream=None):
     _check(lib().kv_read_allocator(pool, rc, ring, ctypes.byref(h), ctypes.byref(t),
                                    _stream(stream)), "kv_read_allocator")
     return list(rc), list(ring), h.value, t.value
+
+
+KERNEL_KINDS = ["alloc", "fork", "release", "compose_meta", "compose_copy", "pack", "unpack",
+                "cow", "qkv", "qkv_decode", "attn", "attn_decode", "merge"]
+
+
+class kv_profile_entry(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
+
+
+def kv_profile_enable(pool, enabled: bool):
+    _check(lib().kv_profile_enable(pool, 1 if enabled else 0), "kv_profile_enable")
+
+
+def kv_profile_read(pool):
+    """{kind: (launches, total_ms)} since the last read."""
+    arr = (kv_profile_entry * len(KERNEL_KINDS))()
+    _check(lib().kv_profile_read(pool, ctypes.cast(arr, ctypes.c_void_p)), "kv_profile_read")
+    return {k: (arr[i].launches, arr[i].total_ms) for i, k in enumerate(KERNEL_KINDS)}
 
 
 class Pool:

@@ -184,3 +184,20 @@ def test_error_codes_on_device(gpu_available):
     assert e.value.status == kv.KV_ERR_EVICTED
     kv.kv_sync(tw.gpu.h)
     tw.close()
+
+
+def test_bf16_fanout_decode_sixteen_agents(gpu_available):
+    """16 agents x 4 query heads share a context: 64 query vectors per KV head in
+    the shared chunks, private tails per agent, chunk boundaries crossed."""
+    base = synth.LLAMA8B_SHAPE
+    shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
+                             base.head_dim, base.block_size, "bf16")
+    tw = Twin(shape, n_blocks=200, max_pos=1200, max_states=24, wl="fan16", check_kv=False)
+    root = tw.materialize(1030)                    # chunks of 512 keys: 3 chunks
+    kids = tw.fork(root, 16)
+    tw.attend(kids, 7)                             # copy-on-write of the shared tail
+    for _ in range(2):
+        tw.attend(kids, 1)
+    tw.attend(kids[3:9], 1)                        # a sub-batch with longer histories
+    tw.attend([root] + kids[:2], 1)
+    tw.close()
