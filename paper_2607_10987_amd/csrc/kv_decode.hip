@@ -31,7 +31,6 @@ constexpr int kTile = 128;       // keys per LDS tile
 constexpr int kLd = kDh + 8;     // K row stride
 constexpr int kVLd = kTile + 8;  // V^T row stride
 constexpr int kPart = kDh + 4;   // floats per partial: m, l, pad, pad, o[128]
-constexpr int kMaxBlk = kCK;     // block ids per member per chunk (block size >= 1)
 
 __device__ inline uint32_t pack2(float a, float b) {
   const __bf16 x = (__bf16)a, y = (__bf16)b;
@@ -43,10 +42,13 @@ template <int RT>
 __global__ void __launch_bounds__(256)
 k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
               float* __restrict__ part, int n_chunks, int l0, float qk_scale_log2) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kTile * kLd];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[kDh * kVLd];
+  constexpr int kKBytes = kTile * kLd * 2, kVBytes = kDh * kVLd * 2;
+  __shared__ __attribute__((aligned(16))) char smem[kKBytes + kVBytes];
+  __shared__ int s_tbl[KV_MAX_BATCH][kCK / 16];
   __shared__ int s_nk[KV_MAX_BATCH], s_lead[KV_MAX_BATCH], s_mem[KV_MAX_BATCH];
   __shared__ int s_nmem;
+  uint16_t* sK = (uint16_t*)smem;
+  uint16_t* sV = (uint16_t*)(smem + kKBytes);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hl = lane >> 5, col = lane & 31;
   const int c = blockIdx.x, gk = blockIdx.y, lc = blockIdx.z;
@@ -54,12 +56,20 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const int b = a.batch;
   const int M = b;  // T == 1
   const int c0 = c * kCK;
+  const int nbc = kCK / g.B;  // table entries per chunk (B divides kCK, B >= 16)
   const uint16_t* pool = (const uint16_t*)g.pool;
+  const int layer = l0 + lc;
 
-  // ---- key counts of each member in this chunk
+  // ---- key counts and block ids of each member in this chunk
   if (tid < b) {
     const int n = a.seq[tid].n_before + 1;
     s_nk[tid] = max(0, min(kCK, n - c0));
+  }
+  for (int i = tid; i < b * nbc; i += 256) {
+    const int sq = i / nbc, j = i % nbc;
+    const int n = a.seq[sq].n_before + 1;
+    const int jb = c0 / g.B + j;
+    s_tbl[sq][j] = jb * g.B < n ? g.tables[(int64_t)a.seq[sq].slot * g.max_blocks + jb] : -1;
   }
   __syncthreads();
   // ---- group members with identical block ids over the chunk (leader = first)
@@ -68,14 +78,12 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     const int nk = s_nk[tid];
     if (nk > 0) {
       const int nb = (nk + g.B - 1) / g.B;
-      const int32_t* t1 = g.tables + (int64_t)a.seq[tid].slot * g.max_blocks + c0 / g.B;
-      for (int s = 0; s < tid; ++s) {
-        if (s_nk[s] != nk) continue;
-        const int32_t* t0 = g.tables + (int64_t)a.seq[s].slot * g.max_blocks + c0 / g.B;
+      for (int sq = 0; sq < tid; ++sq) {
+        if (s_nk[sq] != nk) continue;
         bool same = true;
-        for (int j = 0; j < nb && same; ++j) same = t0[j] == t1[j];
+        for (int j = 0; j < nb; ++j) same &= s_tbl[sq][j] == s_tbl[tid][j];
         if (same) {
-          lead = s;
+          lead = sq;
           break;
         }
       }
@@ -84,19 +92,18 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   }
   __syncthreads();
 
-  const int layer = l0 + lc;
   for (int s0 = 0; s0 < b; ++s0) {
     if (s_lead[s0] != s0 || s_nk[s0] == 0) continue;  // uniform across the workgroup
     if (tid == 0) {
       int n = 0;
-      for (int s = s0; s < b; ++s)
-        if (s_lead[s] == s0) s_mem[n++] = s;
+      for (int sq = s0; sq < b; ++sq)
+        if (s_lead[sq] == s0) s_mem[n++] = sq;
       s_nmem = n;
     }
     __syncthreads();
     const int R = s_nmem * G;  // query vectors of this group (<= 32 RT)
     const int nk = s_nk[s0];
-    const int32_t* trow = g.tables + (int64_t)a.seq[s0].slot * g.max_blocks;
+    const int* tb = s_tbl[s0];
 
     // Q operands: query vector r = member * G + head
     bf16x8 qf[RT][8];
@@ -126,10 +133,9 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 
     const int n_tiles = (nk + kTile - 1) / kTile;
     uint4 rk[8], rv[4][2];
-    auto kaddr = [&](int kk, int kv) -> const uint16_t* {
-      const int key = c0 + kk;
-      const int32_t blk = trow[key / g.B];
-      return pool + (int64_t)blk * g.block_elems + tile_off(g, layer, kv, gk, key % g.B);
+    const int64_t koff = tile_off(g, layer, 0, gk, 0), voff = tile_off(g, layer, 1, gk, 0);
+    auto kaddr = [&](int kk, int64_t base) -> const uint16_t* {
+      return pool + (int64_t)tb[kk / g.B] * g.block_elems + base + (kk % g.B) * kDh;
     };
     auto gload = [&](int t) {
       const int k0 = t * kTile;
@@ -137,14 +143,14 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int i = 0; i < 8; ++i) {
         const int q = tid + 256 * i, r = q >> 4, cc = q & 15;
         const int kk = k0 + r;
-        rk[i] = kk < nk ? *(const uint4*)(kaddr(kk, 0) + cc * 8) : make_uint4(0, 0, 0, 0);
+        rk[i] = kk < nk ? *(const uint4*)(kaddr(kk, koff) + cc * 8) : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int q = tid + 256 * i, kp = q & 63, cc = q >> 6;
         const int kk = k0 + 2 * kp;
-        rv[i][0] = kk < nk ? *(const uint4*)(kaddr(kk, 1) + cc * 8) : make_uint4(0, 0, 0, 0);
-        rv[i][1] = kk + 1 < nk ? *(const uint4*)(kaddr(kk + 1, 1) + cc * 8)
+        rv[i][0] = kk < nk ? *(const uint4*)(kaddr(kk, voff) + cc * 8) : make_uint4(0, 0, 0, 0);
+        rv[i][1] = kk + 1 < nk ? *(const uint4*)(kaddr(kk + 1, voff) + cc * 8)
                                : make_uint4(0, 0, 0, 0);
       }
     };
@@ -230,58 +236,62 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         }
       }
     }
-    __syncthreads();  // LDS tiles free: reuse them for the cross-wave combine
 
     // ---- combine the four wavefronts per query vector, write partials
-    float* sm = (float*)sK;                      // [4 waves][32] m and l
-    float* so = (float*)sV;                      // [32 vectors][128] o, accumulated
-    static_assert(sizeof(sK) >= 2 * 4 * 32 * 4, "combine scratch");
-    static_assert(sizeof(sV) >= 32 * kDh * 4, "combine scratch");
+    float* so = (float*)smem;             // [4 waves][32 vectors][128]
+    float* sm = so + 4 * 32 * kDh;        // [4 waves][32] m, then [4][32] l
+    static_assert(4 * 32 * kDh * 4 + 2 * 4 * 32 * 4 <= kKBytes + kVBytes, "combine scratch");
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
+      __syncthreads();  // LDS tiles (or the previous round) no longer read
       const float lt = l_run[rt] + __shfl_xor(l_run[rt], 32);
       if (hl == 0) {
         sm[wave * 32 + col] = m_run[rt];
         sm[128 + wave * 32 + col] = lt;
       }
-      for (int i = tid; i < 32 * kDh; i += 256) so[i] = 0.f;
-      __syncthreads();
-      float mall = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) mall = fmaxf(mall, sm[w * 32 + col]);
-      const float muse = mall == -INFINITY ? 0.f : mall;
-      const float sc = exp2f(m_run[rt] - muse);
-      for (int w = 0; w < 4; ++w) {
-        if (w == wave) {
+      for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int dc = mt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
-              so[col * kDh + dc] += oacc[rt][mt][e] * sc;
-            }
+        for (int q = 0; q < 4; ++q) {
+          const int dc = mt * 32 + q * 8 + hl * 4;
+          *(float4*)(so + (wave * 32 + col) * kDh + dc) =
+              make_float4(oacc[rt][mt][q * 4], oacc[rt][mt][q * 4 + 1], oacc[rt][mt][q * 4 + 2],
+                          oacc[rt][mt][q * 4 + 3]);
         }
-        __syncthreads();
-      }
-      // write: 32 vectors x (m, l, o[128])
-      for (int i = tid; i < 32 * kDh; i += 256) {
-        const int r = i / kDh, dc = i % kDh;
+      __syncthreads();
+      for (int i = tid; i < 32 * (kDh / 4); i += 256) {
+        const int r = i / (kDh / 4), d4 = (i % (kDh / 4)) * 4;
         const int rr = rt * 32 + r;
         if (rr >= R) continue;
-        const int s = s_mem[rr / G], h = gk * G + rr % G;
-        float* pp = part + ((((int64_t)lc * b + s) * g.Hq + h) * n_chunks + c) * kPart;
-        pp[4 + dc] = so[r * kDh + dc];
-        if (dc == 0) {
-          float m2 = -INFINITY, l2 = 0.f;
-          for (int w = 0; w < 4; ++w) m2 = fmaxf(m2, sm[w * 32 + r]);
-          const float mu = m2 == -INFINITY ? 0.f : m2;
-          for (int w = 0; w < 4; ++w) l2 += sm[128 + w * 32 + r] * exp2f(sm[w * 32 + r] - mu);
+        float mw[4], m2 = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          mw[w] = sm[w * 32 + r];
+          m2 = fmaxf(m2, mw[w]);
+        }
+        const float mu = m2 == -INFINITY ? 0.f : m2;
+        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        float l2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float sc = exp2f(mw[w] - mu);
+          const float4 v = *(const float4*)(so + (w * 32 + r) * kDh + d4);
+          acc4.x += v.x * sc;
+          acc4.y += v.y * sc;
+          acc4.z += v.z * sc;
+          acc4.w += v.w * sc;
+          l2 += sm[128 + w * 32 + r] * sc;
+        }
+        const int sq = s_mem[rr / G], h = gk * G + rr % G;
+        float* pp = part + ((((int64_t)lc * b + sq) * g.Hq + h) * n_chunks + c) * kPart;
+        *(float4*)(pp + 4 + d4) = acc4;
+        if (d4 == 0) {
           pp[0] = m2;
           pp[1] = l2;
         }
       }
-      __syncthreads();
     }
+    __syncthreads();  // partial writes done with the LDS before the next group
   }
 }
 
@@ -317,7 +327,7 @@ int decode_chunks(const AppendDesc& a) { return (a.max_keys + kCK - 1) / kCK; }
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
   const int G = g.Hq / g.Hkv;
   return dtype == KV_DTYPE_BF16 && g.dh == kDh && a.T == 1 && a.batch * G <= 64 &&
-         kCK % g.B == 0 && (kTile % g.B == 0 || g.B % kTile == 0);
+         kCK % g.B == 0 && g.B >= 16;
 }
 
 size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a) {

@@ -260,6 +260,100 @@ k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restric
   }
 }
 
+typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Decode-size projection (M <= 32 token rows): weight streaming.  Each weight
+// element is used by one wavefront only, so operands are loaded straight from
+// global memory in the v_mfma_f32_16x16x32_bf16 layout (a lane reads 16 bytes
+// of one weight row; the four lanes of a row cover 64 contiguous bytes), eight
+// k-steps of loads in flight per lane.  Workgroup = one 128-channel head of one
+// layer, wave w = channels 32 w .. 32 w + 31; RoPE and the stores go through
+// an fp32 tile in LDS.  grid (N / 128, 1, lc), block 256.
+template <int TT>  // token tiles of 16
+__global__ void __launch_bounds__(kThreads)
+k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+             int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
+  constexpr int U = 8;               // k-steps of 32 per batch of loads
+  constexpr int FLD = kDh + 4;
+  __shared__ __attribute__((aligned(16))) float Cf[TT * 16 * FLD];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  const int n0 = blockIdx.x * kDh;
+  const int lc = blockIdx.z, l = l0 + lc;
+  const int M = a.batch * a.T, d = g.d;
+  const uint16_t* wl = w + (int64_t)l * w_stride;
+  const uint16_t* wr0 = wl + (int64_t)(n0 + wave * 32 + lr) * d + lk;
+  const uint16_t* wr1 = wr0 + (int64_t)16 * d;
+  const uint16_t* xr[TT];
+  bool xok[TT];
+#pragma unroll
+  for (int j = 0; j < TT; ++j) {
+    const int row = j * 16 + lr;
+    xok[j] = row < M;
+    xr[j] = x + (int64_t)(xok[j] ? row : 0) * d + lk;
+  }
+  floatx4 acc[2][TT];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < TT; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < d; k0 += 32 * U) {
+    uint4 fa[U][2], fb[U][TT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      fa[u][0] = *(const uint4*)(wr0 + k0 + 32 * u);
+      fa[u][1] = *(const uint4*)(wr1 + k0 + 32 * u);
+#pragma unroll
+      for (int j = 0; j < TT; ++j)
+        fb[u][j] = xok[j] ? *(const uint4*)(xr[j] + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < TT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8v, fa[u][i]), __builtin_bit_cast(bf16x8v, fb[u][j]),
+              acc[i][j], 0, 0, 0);
+  }
+  // C[16 ch x 16 tok]: lane holds channels 4 (lane / 16) + e of token lane % 16
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < TT; ++j) {
+      const int ch = wave * 32 + i * 16 + (lane >> 4) * 4;
+      const int tl = j * 16 + lr;
+      *(float4*)(Cf + tl * FLD + ch) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2],
+                                                   acc[i][j][3]);
+    }
+  __syncthreads();
+  const int half = kDh / 2;
+  const int hh = n0 / kDh;
+  for (int it = tid; it < TT * 16 * (half / 4); it += kThreads) {
+    const int f4 = it % (half / 4), r = it / (half / 4);
+    if (r >= M) continue;
+    const float4 xv = *(const float4*)(Cf + r * FLD + f4 * 4);
+    const float4 yv = *(const float4*)(Cf + r * FLD + half + f4 * 4);
+    float4 xo = xv, yo = yv;
+    if (hh < g.Hq + g.Hkv) {
+      const int pos = row_info(a, r).pos;
+      const float4 cs = *(const float4*)(g.rope_cos + (int64_t)pos * half + f4 * 4);
+      const float4 sn = *(const float4*)(g.rope_sin + (int64_t)pos * half + f4 * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float c = (&cs.x)[q], s = (&sn.x)[q];
+        (&xo.x)[q] = (&xv.x)[q] * c - (&yv.x)[q] * s;
+        (&yo.x)[q] = (&xv.x)[q] * s + (&yv.x)[q] * c;
+      }
+    }
+    uint16_t* dp = dest(g, a, qbuf, lc, l, M, r, hh, f4 * 4);
+    *(uint2*)dp = make_uint2(pack_bf16x2(xo.x, xo.y), pack_bf16x2(xo.z, xo.w));
+    *(uint2*)(dp + half) = make_uint2(pack_bf16x2(yo.x, yo.y), pack_bf16x2(yo.z, yo.w));
+  }
+}
+
 }  // namespace
 
 bool qkv_mfma_ok(const PoolGeom& g, int dtype) {
@@ -271,7 +365,15 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
                            const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s) {
   const int M = a.batch * a.T;
   const int N = (g.Hq + 2 * g.Hkv) * kDh;
-  if (M <= 32) {
+  if (M <= 16 && g.d % 256 == 0) {
+    dim3 grid(N / kDh, 1, lc);
+    k_qkv_decode<1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride,
+                                             a, (uint16_t*)qbuf, l0);
+  } else if (M <= 32 && g.d % 256 == 0) {
+    dim3 grid(N / kDh, 1, lc);
+    k_qkv_decode<2><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride,
+                                             a, (uint16_t*)qbuf, l0);
+  } else if (M <= 32) {
     dim3 grid(N / 128, 1, lc);
     k_qkv_mfma<128, 32, 4, 1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
                                                         w_stride, a, (uint16_t*)qbuf, l0);
