@@ -43,7 +43,7 @@ __device__ inline uint32_t pack2(float a, float b) {
 }
 
 template <int G>
-__global__ void __launch_bounds__(64 * G)
+__global__ void __launch_bounds__(64 * G, 8 / G)
 k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                uint16_t* __restrict__ o, int l0, float qk_scale_log2) {
   constexpr int NT = 64 * G;
@@ -154,14 +154,14 @@ k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
       }
     }
-    // scale, mask, running max
+    // mask, running max on raw scores (scale > 0 commutes with max)
     const bool need_mask = k0 + kKT - 1 > sd.n_before + t0 || k0 + kKT > n_keys || !q_valid;
     float mt_max = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        float s = sacc[kt][e] * qk_scale_log2;
+        float s = sacc[kt][e];
         if (need_mask) {
           const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
           if (kk > uq || kk >= n_keys) s = -INFINITY;
@@ -169,10 +169,14 @@ k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         sacc[kt][e] = s;
         mt_max = fmaxf(mt_max, s);
       }
-    mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32));
-    const float m_new = fmaxf(m_run, mt_max);
+    mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32)) * qk_scale_log2;
+    // Lazy rescaling: the running max only moves when a score exceeds it by
+    // more than 2^8 in the exponent; until then p <= 256, exact in fp32 and
+    // representable in bf16, and O is not rescaled (the final division by l
+    // uses the same reference, so the result is unchanged).
+    const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;  // fully masked (padding) rows
-    const float alpha = exp2f(m_run - m_use);
+    const bool moved = __ballot(m_new != m_run) != 0;
     float psum = 0.f;
     bf16x8 pf[4];  // B operands of the PV product, one per 16-key step
 #pragma unroll
@@ -182,19 +186,23 @@ k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         float p[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          p[j] = exp2f(sacc[kt][hs * 8 + j] - m_use);
+          p[j] = exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
           psum += p[j];
         }
         uint32_t w[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
                          pack2(p[6], p[7])};
         pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(uint4*)w);
       }
-    l_run = l_run * alpha + psum;
+    if (moved) {
+      const float alpha = exp2f(m_run - m_use);
+      l_run *= alpha;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
+    }
+    l_run += psum;
     m_run = m_new;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
     // O^T += V^T P^T; 16-key step s covers keys 16 s + {4h + r, 8 + 4h + r}
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
