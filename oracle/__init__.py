@@ -23,6 +23,6 @@ readings used are listed in each module.
 """
 from .rope import inv_freq, rope_angles, apply_rope, rerotate  # noqa: F401
 from .attention import causal_gqa_attention, attention_rows  # noqa: F401
-from .model import project_qkv, split_w  # noqa: F401
+from .model import project_qkv, project_kv, project_q, split_w  # noqa: F401
 from .pool import (OraclePool, OracleError, Status, Lineage,  # noqa: F401
                    PACK_MAGIC, PACK_VERSION)

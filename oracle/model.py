@@ -27,3 +27,20 @@ def project_qkv(x, w, hq: int, hkv: int, dh: int):
     k = (x @ wk.T).reshape(t, hkv, dh).transpose(1, 0, 2)
     v = (x @ wv.T).reshape(t, hkv, dh).transpose(1, 0, 2)
     return q, k, v
+
+
+def project_kv(x, w, hq: int, hkv: int, dh: int):
+    """Keys and values only: x [T, d] -> k, v [Hkv, T, dh] (no RoPE)."""
+    x = np.asarray(x, dtype=np.float64)
+    _, wk, wv = split_w(w, hq, hkv, dh)
+    t = x.shape[0]
+    k = (x @ wk.T).reshape(t, hkv, dh).transpose(1, 0, 2)
+    v = (x @ wv.T).reshape(t, hkv, dh).transpose(1, 0, 2)
+    return k, v
+
+
+def project_q(x_rows, w, hq: int, hkv: int, dh: int):
+    """Queries of selected token rows: x_rows [R, d] -> q [R, Hq, dh] (no RoPE)."""
+    x_rows = np.asarray(x_rows, dtype=np.float64)
+    wq, _, _ = split_w(w, hq, hkv, dh)
+    return (x_rows @ wq.T).reshape(x_rows.shape[0], hq, dh)

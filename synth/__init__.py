@@ -249,10 +249,11 @@ def to_f64(stored: np.ndarray, dtype: str) -> np.ndarray:
     return np.asarray(stored, dtype=np.float32).astype(np.float64)
 
 
-def normal_torch(key, shape, std: float, dtype: str, device):
+def normal_torch(key, shape, std: float, dtype: str, device, start: int = 0):
     """Same values as :func:`normal_np`, generated by torch on ``device``.
 
-    Returns a float32 or bfloat16 tensor.
+    Elements [start, start + prod(shape)) of the stream; returns a float32 or
+    bfloat16 tensor.
     """
     import torch
     n = int(np.prod(shape))
@@ -265,7 +266,7 @@ def normal_torch(key, shape, std: float, dtype: str, device):
     chunk = 1 << 26
     for s in range(0, n, chunk):
         m = min(chunk, n - s)
-        idx = hash_torch(key, s, m, device) >> 16
+        idx = hash_torch(key, start + s, m, device) >> 16
         out[s:s + m] = tab[idx]
     if dtype == "bf16":
         out = out.view(torch.bfloat16)
@@ -300,3 +301,12 @@ def permutation(seed: int, wl: str, n: int, tag: int = 0) -> np.ndarray:
     rng = np.random.default_rng(np.random.SeedSequence(
         [seed, KIND_PERM, _wl_id(wl), tag]))
     return rng.permutation(n).astype(np.int32)
+
+
+def normal_f64(key, shape, std: float, dtype: str, start: int = 0, device="cpu"):
+    """Float64 values of the stored inputs, generated with torch on ``device``
+    and returned as a host array (the same bits as :func:`normal_np` on any
+    device; faster for large tensors)."""
+    import torch
+    t = normal_torch(key, shape, std, dtype, device, start=start)
+    return t.to(torch.float64).cpu().numpy()

@@ -213,3 +213,16 @@ def test_projection_matches_torch_linear():
 def test_oracle_exports():
     for name in ("OraclePool", "OracleError", "Status", "PACK_MAGIC"):
         assert hasattr(oracle, name)
+
+
+def test_partial_projections_agree_with_full():
+    from oracle import project_kv, project_q
+    hq, hkv, dh, d, t = 4, 2, 8, 24, 5
+    x = RNG.standard_normal((t, d))
+    w = RNG.standard_normal(((hq + 2 * hkv) * dh, d))
+    q, k, v = project_qkv(x, w, hq, hkv, dh)
+    k2, v2 = project_kv(x, w, hq, hkv, dh)
+    q2 = project_q(x[[1, 4]], w, hq, hkv, dh)
+    np.testing.assert_allclose(k2, k, atol=1e-13)
+    np.testing.assert_allclose(v2, v, atol=1e-13)
+    np.testing.assert_allclose(q2, q[:, [1, 4]].transpose(1, 0, 2), atol=1e-13)

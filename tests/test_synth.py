@@ -34,3 +34,12 @@ def test_streams_differ_and_bf16_rounding():
     x = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5], dtype=np.float32)
     assert list(synth.f32_to_bf16_bits(x)) == [0x3F80, 0x3F82, 0xC020]
     assert synth.to_f64(np.array([0x3F80, 0xC020], np.uint16), "bf16").tolist() == [1.0, -2.5]
+
+
+def test_offset_streams_and_f64():
+    key = synth.w_key(0, "tiny", 0)
+    full = synth.normal_np(key, (10, 33), 0.5, "bf16")
+    part = synth.normal_torch(key, (4, 33), 0.5, "bf16", "cpu", start=5 * 33)
+    assert np.array_equal(part.view(torch.int16).numpy(), full[5:9].view(np.int16))
+    f = synth.normal_f64(key, (4, 33), 0.5, "bf16", start=5 * 33)
+    assert np.array_equal(f, synth.to_f64(full[5:9], "bf16"))
