@@ -71,7 +71,7 @@ def kv_bytes_per_token(s):
 
 def cpu_baseline(wl, seed):
     """The float64 oracle on a bounded sample: one layer of the workload's shape,
-    materialize of 2048 context tokens then 8 batched decode steps (batch 4)."""
+    materialize of the whole context, fork, then 16 batched decode steps."""
     import numpy as np
     import synth
     from oracle import OraclePool
@@ -82,7 +82,7 @@ def cpu_baseline(wl, seed):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    T, b, steps = 2048, wl.agents, 8
+    T, b, steps = wl.context, wl.agents, 16
     cols, d = s.qkv_cols, s.d_model
     w = [synth.to_f64(synth.normal_np(synth.w_key(seed, wl.name, 0), (cols, d), s.w_std, s.dtype),
                       s.dtype)]

@@ -26,7 +26,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kDh = 128;
-constexpr int kCK = 512;         // keys per chunk (one workgroup)
+constexpr int kCK = 1024;        // keys per chunk (one workgroup)
 constexpr int kTile = 128;       // keys per LDS tile
 constexpr int kLd = kDh + 8;     // K row stride
 constexpr int kVLd = kTile + 8;  // V^T row stride
@@ -39,12 +39,12 @@ __device__ inline uint32_t pack2(float a, float b) {
 
 // grid (n_chunks, Hkv, lc), block 256.  RT = query-vector tiles of 32.
 template <int RT>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, RT == 1 ? 2 : 1)
 k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
               float* __restrict__ part, int n_chunks, int l0, float qk_scale_log2) {
   constexpr int kKBytes = kTile * kLd * 2, kVBytes = kDh * kVLd * 2;
   __shared__ __attribute__((aligned(16))) char smem[kKBytes + kVBytes];
-  __shared__ int s_tbl[KV_MAX_BATCH][kCK / 16];
+  extern __shared__ int s_tbl_dyn[];  // [batch][kCK / B] block ids of the chunk
   __shared__ int s_nk[KV_MAX_BATCH], s_lead[KV_MAX_BATCH], s_mem[KV_MAX_BATCH];
   __shared__ int s_nmem;
   uint16_t* sK = (uint16_t*)smem;
@@ -57,6 +57,7 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const int M = b;  // T == 1
   const int c0 = c * kCK;
   const int nbc = kCK / g.B;  // table entries per chunk (B divides kCK, B >= 16)
+  auto s_tbl = [&](int sq) -> int* { return s_tbl_dyn + sq * nbc; };
   const uint16_t* pool = (const uint16_t*)g.pool;
   const int layer = l0 + lc;
 
@@ -69,7 +70,7 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     const int sq = i / nbc, j = i % nbc;
     const int n = a.seq[sq].n_before + 1;
     const int jb = c0 / g.B + j;
-    s_tbl[sq][j] = jb * g.B < n ? g.tables[(int64_t)a.seq[sq].slot * g.max_blocks + jb] : -1;
+    s_tbl(sq)[j] = jb * g.B < n ? g.tables[(int64_t)a.seq[sq].slot * g.max_blocks + jb] : -1;
   }
   __syncthreads();
   // ---- group members with identical block ids over the chunk (leader = first)
@@ -81,7 +82,7 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int sq = 0; sq < tid; ++sq) {
         if (s_nk[sq] != nk) continue;
         bool same = true;
-        for (int j = 0; j < nb; ++j) same &= s_tbl[sq][j] == s_tbl[tid][j];
+        for (int j = 0; j < nb; ++j) same &= s_tbl(sq)[j] == s_tbl(tid)[j];
         if (same) {
           lead = sq;
           break;
@@ -103,7 +104,7 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     __syncthreads();
     const int R = s_nmem * G;  // query vectors of this group (<= 32 RT)
     const int nk = s_nk[s0];
-    const int* tb = s_tbl[s0];
+    const int* tb = s_tbl(s0);
 
     // Q operands: query vector r = member * G + head
     bf16x8 qf[RT][8];
@@ -174,12 +175,11 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       }
     };
 
-    gload(0);
     for (int t = 0; t < n_tiles; ++t) {
+      gload(t);         // two workgroups per CU hide each other's load latency
       __syncthreads();  // previous tile fully consumed
       sstore();
       __syncthreads();
-      if (t + 1 < n_tiles) gload(t + 1);
       const int kw = wave * 32;  // this wave's keys within the tile
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
@@ -340,10 +340,13 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   const int nch = decode_chunks(a);
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
   dim3 grid(nch, g.Hkv, lc);
+  const size_t dyn = (size_t)a.batch * (kCK / g.B) * sizeof(int);
   if (a.batch * G <= 32)
-    k_decode_attn<1><<<grid, 256, 0, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0, sc);
+    k_decode_attn<1><<<grid, 256, dyn, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0,
+                                            sc);
   else
-    k_decode_attn<2><<<grid, 256, 0, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0, sc);
+    k_decode_attn<2><<<grid, 256, dyn, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0,
+                                            sc);
   return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@ size_t fast_scratch_bytes(const PoolGeom& g, int dtype, const AppendDesc& a) {
 
 size_t fast_scratch_bound(const kv_model_cfg& c, int64_t, int32_t batch, int64_t max_keys) {
   // split-key partials of a decode call: L x batch x Hq x chunks x (4 + dh) floats
-  const int64_t chunks = (max_keys + 511) / 512;
+  const int64_t chunks = (max_keys + 1023) / 1024;
   return (size_t)c.n_layers * batch * c.n_q_heads * chunks * (c.head_dim + 4) * sizeof(float);
 }
 
