@@ -260,6 +260,159 @@ k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restric
   }
 }
 
+// Prefill projection, main loop with direct global->LDS loads
+// (global_load_lds_dwordx4: lane i of a wavefront writes LDS bytes
+// [16 i, 16 i + 16) of the instruction's 1 KiB destination) and a 4-stage
+// pipeline: three K-steps of 32 are in flight while the fourth is consumed,
+// with no register staging.  Tile 256 channels x 256 tokens, 8 wavefronts of
+// 128 channels x 64 tokens (a wave owns a whole head, so RoPE stays in
+// registers).  LDS rows are 64 bytes (32 k); the 16-byte chunk q of row r is
+// stored at chunk slot q ^ ((r >> 1) & 3) so that the 8 rows an MFMA operand
+// read touches in one LDS cycle hit 8 distinct bank groups.
+constexpr int kDlStages = 4;
+constexpr int kDlBK = 32;
+constexpr int kDlWaves = 8;
+constexpr int kDlThreads = 64 * kDlWaves;
+
+#define KV_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+__global__ void __launch_bounds__(kDlThreads, 1)
+k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+         int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
+  constexpr int CH = 256, BT = 256;
+  constexpr int OP = CH * kDlBK;                 // elements per operand per stage
+  constexpr int STAGE = 2 * OP;
+  constexpr int SLD = CH + 8;                    // epilogue row stride
+  constexpr int MAIN = kDlStages * STAGE * 2;
+  constexpr int EPI = BT * SLD * 2;
+  constexpr int LPW = (OP / 8) / 64 / kDlWaves;  // 1 KiB load instructions per wave per operand
+  constexpr int TI = 4, TJ = 2;
+  __shared__ __attribute__((aligned(16))) char smem_raw[MAIN > EPI ? MAIN : EPI];
+  uint16_t* smem = (uint16_t*)smem_raw;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
+  const int n0 = blockIdx.x * CH;
+  const int m0 = blockIdx.y * BT;
+  const int lc = blockIdx.z, l = l0 + lc;
+  const int M = a.batch * a.T, d = g.d;
+  const uint16_t* wl = w + (int64_t)l * w_stride;
+  const int ch0 = (wave & 1) * 128;        // this wave's head within the tile
+  const int tk0 = (wave >> 1) * (TJ * 32); // this wave's 64 tokens
+
+  const uint16_t* ga[LPW];
+  const uint16_t* gb[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int c = (wave * LPW + j) * 64 + lane, r = c >> 2, q = (c & 3) ^ ((r >> 1) & 3);
+    ga[j] = wl + (int64_t)(n0 + r) * d + q * 8;
+    gb[j] = x + (int64_t)min(m0 + r, M - 1) * d + q * 8;  // rows past M: any valid row
+  }
+  auto issue = [&](int kb, int buf) {
+    uint16_t* As = smem + buf * STAGE;
+    uint16_t* Bs = As + OP;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      __builtin_amdgcn_global_load_lds(ga[j] + kb * kDlBK, KV_LDS(As + (wave * LPW + j) * 512),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gb[j] + kb * kDlBK, KV_LDS(Bs + (wave * LPW + j) * 512),
+                                       16, 0, 0);
+    }
+  };
+
+  floatx16 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = d / kDlBK;
+  for (int st = 0; st < kDlStages - 1 && st < nk; ++st) issue(st, st);
+  for (int kb = 0; kb < nk; ++kb) {
+    // this wave's loads of stage kb are done when at most the two later
+    // stages (2 x 2 LPW instructions) are outstanding; the barrier extends
+    // that to every wave's share of the stage
+    if (kb + kDlStages - 2 < nk)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * 2 * LPW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kb + kDlStages - 1 < nk) issue(kb + kDlStages - 1, (kb + kDlStages - 1) % kDlStages);
+    const uint16_t* As = smem + (kb % kDlStages) * STAGE;
+    const uint16_t* Bs = As + OP;
+#pragma unroll
+    for (int ks = 0; ks < kDlBK / 16; ++ks) {
+      const int q = ks * 2 + hl;
+      bf16x8 fa[TI], fb[TJ];
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int m = ch0 + i * 32 + (lane & 31);
+        fa[i] = *(const bf16x8*)(As + (m * 4 + (q ^ ((m >> 1) & 3))) * 8);
+      }
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) {
+        const int t = tk0 + j * 32 + (lane & 31);
+        fb[j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ ((t >> 1) & 3))) * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  __syncthreads();  // LDS stages become the epilogue's staging tile
+
+  // ---- epilogue: rotate in registers, restage bf16 rows, 16-byte stores
+  const int half = kDh / 2;
+  uint16_t* S = smem;
+  const int hh = (n0 + ch0) / kDh;
+  const bool rot = hh < g.Hq + g.Hkv;
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const int tl = tk0 + j * 32 + (lane & 31);
+    const int row = m0 + tl;
+    const int pos = row < M ? row_info(a, row).pos : 0;
+    const float* cr = g.rope_cos + (int64_t)pos * half;
+    const float* sr = g.rope_sin + (int64_t)pos * half;
+#pragma unroll
+    for (int i = 0; i < TI / 2; ++i) {
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int f0 = i * 32 + e4 * 8 + hl * 4;
+        float4 cs = make_float4(1.f, 1.f, 1.f, 1.f), sn = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (rot) {
+          cs = *(const float4*)(cr + f0);
+          sn = *(const float4*)(sr + f0);
+        }
+        float xr[4], yr[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float xv = acc[i][j][e4 * 4 + q], yv = acc[i + 2][j][e4 * 4 + q];
+          const float c = (&cs.x)[q], s = (&sn.x)[q];
+          xr[q] = xv * c - yv * s;
+          yr[q] = xv * s + yv * c;
+        }
+        *(uint2*)(S + tl * SLD + ch0 + f0) =
+            make_uint2(pack_bf16x2(xr[0], xr[1]), pack_bf16x2(xr[2], xr[3]));
+        *(uint2*)(S + tl * SLD + ch0 + half + f0) =
+            make_uint2(pack_bf16x2(yr[0], yr[1]), pack_bf16x2(yr[2], yr[3]));
+      }
+    }
+  }
+  __syncthreads();
+  constexpr int G8 = CH / 8;
+  for (int q = tid; q < BT * G8; q += kDlThreads) {
+    const int r = q / G8, c8 = q % G8;
+    const int row = m0 + r;
+    if (row >= M) continue;
+    const uint4 v = *(const uint4*)(S + r * SLD + c8 * 8);
+    const int ch = n0 + c8 * 8;
+    *(uint4*)dest(g, a, qbuf, lc, l, M, row, ch / kDh, ch % kDh) = v;
+  }
+}
+
 typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -377,6 +530,10 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
     dim3 grid(N / 128, 1, lc);
     k_qkv_mfma<128, 32, 4, 1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
                                                         w_stride, a, (uint16_t*)qbuf, l0);
+  } else if (g.d % kDlBK == 0) {
+    dim3 grid(N / 256, (M + 255) / 256, lc);
+    k_qkv_dl<<<grid, kDlThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a,
+                                          (uint16_t*)qbuf, l0);
   } else {
     dim3 grid(N / 256, (M + 255) / 256, lc);
     k_qkv_mfma<256, 256, 2, 2><<<grid, kThreads, 0, s>>>(
