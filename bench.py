@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--decode", type=int, default=None, help="override decode steps")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device copy first (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -168,6 +170,13 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] setup done in {time.perf_counter() - t_setup:.1f} s", file=sys.stderr,
           flush=True)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     info = {}
 

@@ -161,6 +161,9 @@ struct kv_pool {
     g.B = cfg.block_size;
     g.d = cfg.d_model;
     g.max_pos = cfg.max_pos;
+    g.b_shift = -1;
+    for (int sh = 0; sh < 7; ++sh)
+      if ((1 << sh) == cfg.block_size) g.b_shift = sh;
     return g;
   }
   int64_t free_blocks() const { return tail - head; }

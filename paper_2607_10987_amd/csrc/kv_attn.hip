@@ -20,6 +20,7 @@
 // same key order.  Softmax: running max / running sum per token in base 2
 // (scores pre-multiplied by log2(e) / sqrt(dh)), halves of a token combined
 // with one lane swap.
+#include "kv_dma.h"
 #include "kv_fast.h"
 
 namespace kvs {
@@ -239,7 +240,8 @@ k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 // ---------------------------------------------------------------------------
 // Pipelined variant: K and V tiles stream straight from the paged pool into
 // LDS (global_load_lds_dwordx4, three tiles in flight), unpadded 256-byte key
-// rows with the 16-byte chunk c of row r stored at slot c ^ (r & 7).  V stays
+// rows with the 16-byte chunk c of row r stored at slot c ^ (r & 15), so that
+// 16 consecutive rows read at one chunk hit 16 distinct bank groups.  V stays
 // in key-major order; its MFMA operand (4 consecutive keys of one channel per
 // half) is read with ds_read_b64_tr_b16: within each group of 16 lanes, lane
 // i addressing row key0 + i / 4, channels c0 + 4 (i % 4) .. + 3 receives the
@@ -251,7 +253,6 @@ constexpr int kPS = 3;                 // pipeline stages
 constexpr int kPTile = kKT * kDh;      // elements of one K (or V) tile
 
 typedef short v4s __attribute__((ext_vector_type(4)));
-#define KV_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 #define KV_LDS4(p) ((__attribute__((address_space(3))) v4s*)(p))
 
 template <int G>
@@ -294,6 +295,8 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     const uint16_t* qp = qbuf + (((int64_t)lc * M + row) * g.Hq + h) * kDh;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) qf[ks] = *(const bf16x8*)(qp + ks * 16 + hl * 8);
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) settle(qf[ks]);
   }
   __syncthreads();  // s_tbl ready
 
@@ -307,11 +310,12 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     for (int jj = 0; jj < 2; ++jj) {
       const int j = wave + jj * kPW;
       const int r = j * 4 + (lane >> 4);
-      const int c = (lane & 15) ^ (r & 7);
+      const int c = (lane & 15) ^ (r & 15);
       const int key = min(tile * kKT + r, key_end - 1);  // rows past the end: any staged key
-      const int64_t base = (int64_t)s_tbl[key / g.B] * g.block_elems + (key % g.B) * kDh + c * 8;
-      __builtin_amdgcn_global_load_lds(pool + base + koff, KV_LDS(Ks + j * 512), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(pool + base + voff, KV_LDS(Vs + j * 512), 16, 0, 0);
+      const int64_t base = (int64_t)s_tbl[key >> g.b_shift] * g.block_elems +
+                           (key & (g.B - 1)) * kDh + c * 8;
+      lds_dma16(pool + base + koff, Ks + j * 512);
+      lds_dma16(pool + base + voff, Vs + j * 512);
     }
   };
 
@@ -325,10 +329,10 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
   for (int tile = 0; tile < n_tiles; ++tile) {
     if (tile + 1 < n_tiles)
-      asm volatile("s_waitcnt vmcnt(4)" ::: "memory");  // the next tile (4 loads) may be pending
+      wait_vmcnt<4>();  // the next tile (4 copies per wave) may be pending
     else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+      wait_vmcnt<0>();
+    lds_barrier();
     if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
     const uint16_t* Ks = smem + (tile % kPS) * 2 * kPTile;
     const uint16_t* Vs = Ks + kPTile;
@@ -342,12 +346,13 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       const int r = kt * 32 + col;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ (r & 7)) * 8));
+        const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ (r & 15)) * 8));
         sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
       }
     }
+    // wave-uniform: does any (query, key) pair of this tile need masking?
     const bool need_mask = k0 + kKT - 1 > sd.n_before + t0 + tg * 32 || k0 + kKT > n_keys ||
-                           !q_valid;
+                           t0 + tg * 32 + 31 >= a.T;
     float mt_max = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -364,7 +369,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32)) * qk_scale_log2;
     const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const bool moved = __ballot(m_new != m_run) != 0;
+    const bool moved = __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run) != 0)) != 0;
     float psum = 0.f;
     bf16x8 pf[4];
 #pragma unroll
@@ -374,7 +379,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         float p[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          p[j] = exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
+          p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
           psum += p[j];
         }
         uint32_t wv[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
@@ -382,7 +387,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(uint4*)wv);
       }
     if (moved) {
-      const float alpha = exp2f(m_run - m_use);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
       l_run *= alpha;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
@@ -401,10 +406,10 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const int dc = mt * 32 + (gi & 1) * 16 + (li & 3) * 4;
         const int ch = dc >> 3, hf = (dc & 7);
         const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_a * kDh + ((ch ^ (key_a & 7)) * 8) + hf));
+            KV_LDS4(Vs + key_a * kDh + ((ch ^ (key_a & 15)) * 8) + hf));
         const int key_b = key_a + 8;
         const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_b * kDh + ((ch ^ (key_b & 7)) * 8) + hf));
+            KV_LDS4(Vs + key_b * kDh + ((ch ^ (key_b & 15)) * 8) + hf));
         const v4s vv[2] = {r0, r1};
         oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf[s4],
                                                            oacc[mt], 0, 0, 0);
@@ -431,7 +436,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 
 bool attn_mfma_ok(const PoolGeom& g, int dtype) {
   const int G = g.Hq / g.Hkv;
-  return dtype == KV_DTYPE_BF16 && g.dh == kDh && (G == 4 || G == 8);
+  return dtype == KV_DTYPE_BF16 && g.dh == kDh && (G == 4 || G == 8) && g.b_shift >= 0;
 }
 
 hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const AppendDesc& a, void* o,

@@ -1,0 +1,48 @@
+// Asynchronous global -> LDS copies for multi-stage pipelines (gfx950).
+//
+// lds_dma16 issues global_load_lds_dwordx4: lane i of the wavefront copies 16
+// bytes from its global address to LDS bytes [16 i, 16 i + 16) after the
+// wave-uniform LDS base `lds`.  It is written as inline assembly so that the
+// compiler does not track the copy; the pipelines order it explicitly:
+//   * wait_vmcnt<N>() (s_waitcnt vmcnt(N)) before reading a stage: the wave's
+//     copies complete in issue order, so all but its N most recent are done;
+//   * lds_barrier() (s_waitcnt lgkmcnt(0); s_barrier), a workgroup barrier
+//     without the memory fence of __syncthreads(), whose vmcnt(0) would drain
+//     every stage in flight.  After it, every wave's copies of the stage are
+//     visible and every wave has finished reading the buffer about to be
+//     refilled.  The "memory" clobbers keep the compiler from moving memory
+//     accesses across either statement.
+// Values loaded with ordinary global loads before a pipeline must be made
+// ready with settle() so that the compiler's own wait for them is not placed
+// inside the pipelined loop (where it would wait for every copy as well).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvs {
+
+__device__ inline void lds_dma16(const void* gptr, void* lds) {
+  const uint32_t la = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(la)
+               : "memory", "m0");
+}
+
+template <int N>
+__device__ inline void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ inline void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <typename T>
+__device__ inline void settle(T& v) {
+  asm volatile("" : "+v"(v));
+}
+
+}  // namespace kvs

@@ -19,6 +19,7 @@
 //            four waves of 32 channels, fp32 tile in LDS for the rotation.
 // Q goes to the scratch buffer [lc][M][Hq * dh]; K and V rows go to
 // pool[table[slot][u / B]][l][K|V][kv head][u % B][:] with u = n_before + t.
+#include "kv_dma.h"
 #include "kv_fast.h"
 
 namespace kvs {
@@ -267,14 +268,15 @@ k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restric
 // with no register staging.  Tile 256 channels x 256 tokens, 8 wavefronts of
 // 128 channels x 64 tokens (a wave owns a whole head, so RoPE stays in
 // registers).  LDS rows are 64 bytes (32 k); the 16-byte chunk q of row r is
-// stored at chunk slot q ^ ((r >> 1) & 3) so that the 8 rows an MFMA operand
-// read touches in one LDS cycle hit 8 distinct bank groups.
+// stored at chunk slot q ^ f(r), f(r) = ((r >> 1) ^ (r >> 3)) & 3, so that
+// the consecutive rows an MFMA operand read serves in one LDS cycle (8 rows
+// with 32 banks, 16 rows with 64 banks) land in distinct bank groups.
+__device__ inline int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
 constexpr int kDlStages = 4;
 constexpr int kDlBK = 32;
 constexpr int kDlWaves = 8;
 constexpr int kDlThreads = 64 * kDlWaves;
-
-#define KV_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
 __global__ void __launch_bounds__(kDlThreads, 1)
 k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
@@ -303,7 +305,7 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
   const uint16_t* gb[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
-    const int c = (wave * LPW + j) * 64 + lane, r = c >> 2, q = (c & 3) ^ ((r >> 1) & 3);
+    const int c = (wave * LPW + j) * 64 + lane, r = c >> 2, q = (c & 3) ^ swz(r);
     ga[j] = wl + (int64_t)(n0 + r) * d + q * 8;
     gb[j] = x + (int64_t)min(m0 + r, M - 1) * d + q * 8;  // rows past M: any valid row
   }
@@ -312,10 +314,8 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
     uint16_t* Bs = As + OP;
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
-      __builtin_amdgcn_global_load_lds(ga[j] + kb * kDlBK, KV_LDS(As + (wave * LPW + j) * 512),
-                                       16, 0, 0);
-      __builtin_amdgcn_global_load_lds(gb[j] + kb * kDlBK, KV_LDS(Bs + (wave * LPW + j) * 512),
-                                       16, 0, 0);
+      lds_dma16(ga[j] + kb * kDlBK, As + (wave * LPW + j) * 512);
+      lds_dma16(gb[j] + kb * kDlBK, Bs + (wave * LPW + j) * 512);
     }
   };
 
@@ -334,10 +334,10 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
     // stages (2 x 2 LPW instructions) are outstanding; the barrier extends
     // that to every wave's share of the stage
     if (kb + kDlStages - 2 < nk)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * 2 * LPW) : "memory");
+      wait_vmcnt<2 * 2 * LPW>();
     else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+      wait_vmcnt<0>();
+    lds_barrier();
     if (kb + kDlStages - 1 < nk) issue(kb + kDlStages - 1, (kb + kDlStages - 1) % kDlStages);
     const uint16_t* As = smem + (kb % kDlStages) * STAGE;
     const uint16_t* Bs = As + OP;
@@ -348,12 +348,12 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
 #pragma unroll
       for (int i = 0; i < TI; ++i) {
         const int m = ch0 + i * 32 + (lane & 31);
-        fa[i] = *(const bf16x8*)(As + (m * 4 + (q ^ ((m >> 1) & 3))) * 8);
+        fa[i] = *(const bf16x8*)(As + (m * 4 + (q ^ swz(m))) * 8);
       }
 #pragma unroll
       for (int j = 0; j < TJ; ++j) {
         const int t = tk0 + j * 32 + (lane & 31);
-        fb[j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ ((t >> 1) & 3))) * 8);
+        fb[j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ swz(t))) * 8);
       }
 #pragma unroll
       for (int i = 0; i < TI; ++i)
@@ -419,16 +419,20 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // Decode-size projection (M <= 32 token rows): weight streaming.  Each weight
 // element is used by one wavefront only, so operands are loaded straight from
 // global memory in the v_mfma_f32_16x16x32_bf16 layout (a lane reads 16 bytes
-// of one weight row; the four lanes of a row cover 64 contiguous bytes), eight
-// k-steps of loads in flight per lane.  Workgroup = one 128-channel head of one
-// layer, wave w = channels 32 w .. 32 w + 31; RoPE and the stores go through
-// an fp32 tile in LDS.  grid (N / 128, 1, lc), block 256.
+// of one weight row; the four lanes of a row cover 64 contiguous bytes),
+// sixteen k-steps of loads in flight per lane.  Workgroup = one 128-channel
+// head of one layer, eight waves of 16 channels (so that the launch, 1536
+// workgroups for the 8B shape, fills the GPU in whole rounds); RoPE and the
+// stores go through an fp32 tile in LDS.  grid (N / 128, 1, lc), block 512.
+constexpr int kDecWaves = 8;
+
 template <int TT>  // token tiles of 16
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(64 * kDecWaves)
 k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
              int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
-  constexpr int U = 8;               // k-steps of 32 per batch of loads
+  constexpr int U = 16;              // k-steps of 32 per batch of loads
   constexpr int FLD = kDh + 4;
+  constexpr int NT = 64 * kDecWaves;
   __shared__ __attribute__((aligned(16))) float Cf[TT * 16 * FLD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lk = (lane >> 4) * 8;
@@ -436,8 +440,7 @@ k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restr
   const int lc = blockIdx.z, l = l0 + lc;
   const int M = a.batch * a.T, d = g.d;
   const uint16_t* wl = w + (int64_t)l * w_stride;
-  const uint16_t* wr0 = wl + (int64_t)(n0 + wave * 32 + lr) * d + lk;
-  const uint16_t* wr1 = wr0 + (int64_t)16 * d;
+  const uint16_t* wr = wl + (int64_t)(n0 + wave * 16 + lr) * d + lk;
   const uint16_t* xr[TT];
   bool xok[TT];
 #pragma unroll
@@ -446,17 +449,14 @@ k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restr
     xok[j] = row < M;
     xr[j] = x + (int64_t)(xok[j] ? row : 0) * d + lk;
   }
-  floatx4 acc[2][TT];
+  floatx4 acc[TT];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < TT; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < TT; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0; k0 < d; k0 += 32 * U) {
-    uint4 fa[U][2], fb[U][TT];
+    uint4 fa[U], fb[U][TT];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      fa[u][0] = *(const uint4*)(wr0 + k0 + 32 * u);
-      fa[u][1] = *(const uint4*)(wr1 + k0 + 32 * u);
+      fa[u] = *(const uint4*)(wr + k0 + 32 * u);
 #pragma unroll
       for (int j = 0; j < TT; ++j)
         fb[u][j] = xok[j] ? *(const uint4*)(xr[j] + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
@@ -464,27 +464,22 @@ k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restr
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < TT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8v, fa[u][i]), __builtin_bit_cast(bf16x8v, fb[u][j]),
-              acc[i][j], 0, 0, 0);
+      for (int j = 0; j < TT; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa[u]),
+                                                         __builtin_bit_cast(bf16x8v, fb[u][j]),
+                                                         acc[j], 0, 0, 0);
   }
   // C[16 ch x 16 tok]: lane holds channels 4 (lane / 16) + e of token lane % 16
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < TT; ++j) {
-      const int ch = wave * 32 + i * 16 + (lane >> 4) * 4;
-      const int tl = j * 16 + lr;
-      *(float4*)(Cf + tl * FLD + ch) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2],
-                                                   acc[i][j][3]);
-    }
+  for (int j = 0; j < TT; ++j) {
+    const int ch = wave * 16 + (lane >> 4) * 4;
+    const int tl = j * 16 + lr;
+    *(float4*)(Cf + tl * FLD + ch) = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+  }
   __syncthreads();
   const int half = kDh / 2;
   const int hh = n0 / kDh;
-  for (int it = tid; it < TT * 16 * (half / 4); it += kThreads) {
+  for (int it = tid; it < TT * 16 * (half / 4); it += NT) {
     const int f4 = it % (half / 4), r = it / (half / 4);
     if (r >= M) continue;
     const float4 xv = *(const float4*)(Cf + r * FLD + f4 * 4);
@@ -518,14 +513,14 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
                            const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s) {
   const int M = a.batch * a.T;
   const int N = (g.Hq + 2 * g.Hkv) * kDh;
-  if (M <= 16 && g.d % 256 == 0) {
+  if (M <= 16 && g.d % 512 == 0) {
     dim3 grid(N / kDh, 1, lc);
-    k_qkv_decode<1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride,
-                                             a, (uint16_t*)qbuf, l0);
-  } else if (M <= 32 && g.d % 256 == 0) {
+    k_qkv_decode<1><<<grid, 64 * kDecWaves, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
+                                                   w_stride, a, (uint16_t*)qbuf, l0);
+  } else if (M <= 32 && g.d % 512 == 0) {
     dim3 grid(N / kDh, 1, lc);
-    k_qkv_decode<2><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride,
-                                             a, (uint16_t*)qbuf, l0);
+    k_qkv_decode<2><<<grid, 64 * kDecWaves, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
+                                                   w_stride, a, (uint16_t*)qbuf, l0);
   } else if (M <= 32) {
     dim3 grid(N / 128, 1, lc);
     k_qkv_mfma<128, 32, 4, 1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,

@@ -31,6 +31,7 @@ struct PoolGeom {
   int32_t max_blocks;
   int32_t L, Hq, Hkv, dh, B, d;
   int32_t max_pos;
+  int32_t b_shift;  // log2(B) when B is a power of two, else -1
 };
 
 // Element offset of (layer, K|V, kv head, slot, channel 0) inside a block.
