@@ -2,20 +2,24 @@
 // split over key chunks, reading each shared block once for the whole batch.
 //
 // Forked agents share the blocks of their common context (same physical ids
-// in their block tables).  A workgroup owns one chunk of 512 key positions of
-// one (layer, KV head); it groups the batch members whose block ids and key
-// counts agree over the chunk, and for each group streams the chunk's K/V once
-// while computing the scores of all of the group's query vectors (members x
-// the G query heads of the KV head) with MFMA.  Per (query vector, chunk) it
-// writes a partial (running max m, running sum l, unnormalised output o);
-// k_decode_merge combines the chunks with the usual log-sum-exp rescaling.
+// in their block tables).  The keys of a decode step are cut into chunks of
+// kCK positions.  k_decode_plan (one wavefront per chunk) groups the batch
+// members whose key counts and block ids agree over the chunk; each group of
+// a chunk is one work unit.  The grouping is the same for every layer and KV
+// head, so it is computed once per call.
 //
-// Inside a workgroup the chunk is walked in 4 tiles of 128 keys staged in LDS
-// (K rows, V transposed on the way in, next tile prefetched into registers);
-// wavefront w takes keys 32 w .. 32 w + 31 of each tile for every query
-// vector, and the four wavefronts' partials are combined in LDS at the end.
-// The MFMA products use the same transposed layout as the prefill kernel
-// (query vector in the MFMA column, softmax state lane-local).
+// k_decode_stream runs one wavefront per (unit, KV head, layer) with no
+// workgroup barriers: it streams the unit's K/V rows once, 32 keys at a time,
+// through a ring of LDS stages filled by direct global->LDS copies, and scores
+// all of the group's query vectors (members x the G query heads of the KV
+// head) with MFMA in the transposed layout of the prefill kernel (query vector
+// in the MFMA column, softmax state lane-local, V^T operands by transposed LDS
+// reads).  Per (query vector, chunk) it writes a partial (running max m,
+// running sum l, unnormalised output o); k_decode_merge combines the chunks of
+// a query with the usual log-sum-exp rescaling.
+#include <algorithm>
+
+#include "kv_dma.h"
 #include "kv_fast.h"
 
 namespace kvs {
@@ -24,101 +28,186 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+#define KV_LDS4(p) ((__attribute__((address_space(3))) v4s*)(p))
 
 constexpr int kDh = 128;
-constexpr int kCK = 1024;        // keys per chunk (one workgroup)
-constexpr int kTile = 128;       // keys per LDS tile
-constexpr int kLd = kDh + 8;     // K row stride
-constexpr int kVLd = kTile + 8;  // V^T row stride
-constexpr int kPart = kDh + 4;   // floats per partial: m, l, pad, pad, o[128]
+constexpr int kCK = 1024;              // keys per chunk
+constexpr int kKT = 32;                // keys per pipeline stage
+constexpr int kStage = 2 * kKT * kDh;  // elements per stage: K rows, then V rows
+constexpr int kPart = kDh + 4;         // floats per partial: m, l, pad, pad, o[128]
+
+// One work unit: the members in `mask` share block ids and key count `nk`
+// over the chunk; `lead` is the first of them.
+struct DecodeUnit {
+  int32_t lead, nk;
+  uint32_t mask_lo, mask_hi;
+};
 
 __device__ inline uint32_t pack2(float a, float b) {
   const __bf16 x = (__bf16)a, y = (__bf16)b;
   return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
 }
 
-// grid (n_chunks, Hkv, lc), block 256.  RT = query-vector tiles of 32.
-template <int RT>
-__global__ void __launch_bounds__(256, RT == 1 ? 2 : 1)
-k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
-              float* __restrict__ part, int n_chunks, int l0, float qk_scale_log2) {
-  constexpr int kKBytes = kTile * kLd * 2, kVBytes = kDh * kVLd * 2;
-  __shared__ __attribute__((aligned(16))) char smem[kKBytes + kVBytes];
-  extern __shared__ int s_tbl_dyn[];  // [batch][kCK / B] block ids of the chunk
-  __shared__ int s_nk[KV_MAX_BATCH], s_lead[KV_MAX_BATCH], s_mem[KV_MAX_BATCH];
-  __shared__ int s_nmem;
-  uint16_t* sK = (uint16_t*)smem;
-  uint16_t* sV = (uint16_t*)(smem + kKBytes);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hl = lane >> 5, col = lane & 31;
-  const int c = blockIdx.x, gk = blockIdx.y, lc = blockIdx.z;
-  const int G = g.Hq / g.Hkv;
-  const int b = a.batch;
-  const int M = b;  // T == 1
+// grid (n_chunks), block 64; dynamic LDS: batch * (kCK / B) ints.
+// Writes the units of chunk c to units[c * batch ...] and their number to
+// n_units[c].
+__global__ void __launch_bounds__(64)
+k_decode_plan(PoolGeom g, AppendDesc a, DecodeUnit* __restrict__ units,
+              int* __restrict__ n_units) {
+  extern __shared__ int s_rows[];  // [batch][kCK / B]: each member's block ids in the chunk
+  const int lane = threadIdx.x, c = blockIdx.x, b = a.batch;
   const int c0 = c * kCK;
-  const int nbc = kCK / g.B;  // table entries per chunk (B divides kCK, B >= 16)
-  auto s_tbl = [&](int sq) -> int* { return s_tbl_dyn + sq * nbc; };
-  const uint16_t* pool = (const uint16_t*)g.pool;
-  const int layer = l0 + lc;
-
-  // ---- key counts and block ids of each member in this chunk
-  if (tid < b) {
-    const int n = a.seq[tid].n_before + 1;
-    s_nk[tid] = max(0, min(kCK, n - c0));
+  const int nbc = kCK >> g.b_shift, nbs = __builtin_ctz(nbc);
+  const int jb0 = c0 >> g.b_shift;
+  for (int i = lane; i < b * nbc; i += 64) {
+    const int m = i >> nbs, jb = jb0 + (i & (nbc - 1));
+    const int n = a.seq[m].n_before + 1;
+    s_rows[i] = (jb << g.b_shift) < n ? g.tables[(int64_t)a.seq[m].slot * g.max_blocks + jb] : -1;
   }
-  for (int i = tid; i < b * nbc; i += 256) {
-    const int sq = i / nbc, j = i % nbc;
-    const int n = a.seq[sq].n_before + 1;
-    const int jb = c0 / g.B + j;
-    s_tbl(sq)[j] = jb * g.B < n ? g.tables[(int64_t)a.seq[sq].slot * g.max_blocks + jb] : -1;
-  }
+  const int nk_l = lane < b ? max(0, min(kCK, a.seq[lane].n_before + 1 - c0)) : 0;
   __syncthreads();
-  // ---- group members with identical block ids over the chunk (leader = first)
-  if (tid < b) {
-    int lead = tid;
-    const int nk = s_nk[tid];
-    if (nk > 0) {
-      const int nb = (nk + g.B - 1) / g.B;
-      for (int sq = 0; sq < tid; ++sq) {
-        if (s_nk[sq] != nk) continue;
-        bool same = true;
-        for (int j = 0; j < nb; ++j) same &= s_tbl(sq)[j] == s_tbl(tid)[j];
-        if (same) {
-          lead = sq;
-          break;
-        }
+  // lane q describes group q: leader, key count, first block id, members
+  int n_groups = 0, g_lead = 0, g_nk = 0, g_first = 0;
+  uint64_t g_mask = 0;
+  for (int m = 0; m < b; ++m) {
+    const int nk = __shfl(nk_l, m);
+    if (nk == 0) continue;
+    const int first = s_rows[m * nbc];
+    const int nb = (nk + g.B - 1) >> g.b_shift;
+    uint64_t cand = __ballot(lane < n_groups && g_nk == nk && g_first == first);
+    int found = -1;
+    while (cand) {
+      const int q = __builtin_ctzll(cand);
+      const int lead = __shfl(g_lead, q);
+      const bool diff = lane < nb && s_rows[lead * nbc + lane] != s_rows[m * nbc + lane];
+      if (__ballot(diff) == 0) {
+        found = q;
+        break;
+      }
+      cand &= cand - 1;
+    }
+    if (found < 0) {
+      found = n_groups++;
+      if (lane == found) {
+        g_lead = m;
+        g_nk = nk;
+        g_first = first;
+        g_mask = 0;
       }
     }
-    s_lead[tid] = lead;
+    if (lane == found) g_mask |= 1ull << m;
   }
-  __syncthreads();
+  if (lane < n_groups)
+    units[c * b + lane] = DecodeUnit{g_lead, g_nk, (uint32_t)g_mask, (uint32_t)(g_mask >> 32)};
+  if (lane == 0) n_units[c] = n_groups;
+}
 
-  for (int s0 = 0; s0 < b; ++s0) {
-    if (s_lead[s0] != s0 || s_nk[s0] == 0) continue;  // uniform across the workgroup
-    if (tid == 0) {
-      int n = 0;
-      for (int sq = s0; sq < b; ++sq)
-        if (s_lead[sq] == s0) s_mem[n++] = sq;
-      s_nmem = n;
+// Which chunk holds unit u of the concatenated per-chunk unit lists, and the
+// unit's index within it.  Wave-uniform.
+__device__ inline void locate_unit(const int* __restrict__ n_units, int n_chunks, int u,
+                                   int* chunk, int* idx) {
+  const int lane = threadIdx.x & 63;
+  int run = 0;
+  *chunk = -1;
+  for (int cb = 0; cb < n_chunks; cb += 64) {
+    const int v = cb + lane < n_chunks ? n_units[cb + lane] : 0;
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int t = __shfl_up(inc, d);
+      if (lane >= d) inc += t;
     }
-    __syncthreads();
-    const int R = s_nmem * G;  // query vectors of this group (<= 32 RT)
-    const int nk = s_nk[s0];
-    const int* tb = s_tbl(s0);
+    const uint64_t hit = __ballot(v > 0 && run + inc - v <= u && u < run + inc);
+    if (hit) {
+      const int q = __builtin_ctzll(hit);
+      *chunk = cb + q;
+      *idx = u - run - __shfl(inc - v, q);
+      return;
+    }
+    run += __shfl(inc, 63);
+  }
+}
 
-    // Q operands: query vector r = member * G + head
+// grid (slots, Hkv, lc), block 64.  Workgroup x takes units x, x + slots, ...
+// RT = query-vector tiles of 32 (a unit has at most 32 RT vectors); S = LDS
+// stages (S - 1 in flight while one is consumed).
+template <int RT, int S>
+__global__ void __launch_bounds__(64)
+k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
+                const DecodeUnit* __restrict__ units, const int* __restrict__ n_units,
+                float* __restrict__ part, int n_chunks, int l0, float qk_scale_log2) {
+  static_assert(S >= 2 && S <= 4, "stages");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[S * kStage];
+  const int lane = threadIdx.x, hl = lane >> 5, col = lane & 31;
+  const int gk = blockIdx.y, lc = blockIdx.z, layer = l0 + lc;
+  const int G = g.Hq / g.Hkv, b = a.batch, M = b;  // T == 1
+  const uint16_t* pool = (const uint16_t*)g.pool;
+  const int64_t koff = tile_off(g, layer, 0, gk, 0), voff = tile_off(g, layer, 1, gk, 0);
+
+  int total = 0;
+  for (int cb = 0; cb < n_chunks; cb += 64) {
+    int v = cb + lane < n_chunks ? n_units[cb + lane] : 0;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
+    total += v;
+  }
+
+  for (int u = blockIdx.x; u < total; u += gridDim.x) {
+    int c, gi;
+    locate_unit(n_units, n_chunks, u, &c, &gi);
+    const DecodeUnit un = units[c * b + gi];
+    const int nk = un.nk;
+    const uint64_t mask = ((uint64_t)un.mask_hi << 32) | un.mask_lo;
+    const int R = __popcll(mask) * G;  // query vectors of the unit
+    const bool two = RT > 1 && R > 32;
+    const int c0 = c * kCK;
+    // lane j: block id of the leader's entry j of the chunk
+    const int tbl = (lane << g.b_shift) < nk
+                        ? g.tables[(int64_t)a.seq[un.lead].slot * g.max_blocks +
+                                   (c0 >> g.b_shift) + lane]
+                        : 0;
+
+    // Q^T operands: query vector r = (member rank) * G + head
     bf16x8 qf[RT][8];
+    int qrow[RT], qhead[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int r = rt * 32 + col;
       const bool ok = r < R;
-      const int mi = ok ? r / G : 0, w = ok ? r % G : 0;
-      const int row = s_mem[mi];
-      const uint16_t* qp = qbuf + (((int64_t)lc * M + row) * g.Hq + gk * G + w) * kDh;
+      const int mi = ok ? r / G : 0;
+      uint64_t mm = mask;
+      for (int i = 0; i < mi; ++i) mm &= mm - 1;
+      qrow[rt] = ok ? __builtin_ctzll(mm) : -1;
+      qhead[rt] = gk * G + (ok ? r - mi * G : 0);
+      const uint16_t* qp = qbuf + (((int64_t)lc * M + (ok ? qrow[rt] : 0)) * g.Hq + qhead[rt]) * kDh;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks)
         qf[rt][ks] = ok ? *(const bf16x8*)(qp + ks * 16 + hl * 8) : bf16x8{};
     }
+    int tb = tbl;
+    settle(tb);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) settle(qf[rt][ks]);
+
+    // stage loads: 8 copies of 1 KiB (4 key rows) per operand; rows past the
+    // unit's last key repeat that key, whose score is masked
+    auto issue = [&](int tile, int buf) {
+      uint16_t* Ks = smem + buf * kStage;
+      uint16_t* Vs = Ks + kKT * kDh;
+#pragma unroll
+      for (int j = 0; j < kKT / 4; ++j) {
+        const int r = j * 4 + (lane >> 4);
+        const int cc = (lane & 15) ^ (r & 15);
+        const int key = min(tile * kKT + r, nk - 1);
+        const int id = __shfl(tb, key >> g.b_shift);
+        const int64_t base = (int64_t)id * g.block_elems + (key & (g.B - 1)) * kDh + cc * 8;
+        lds_dma16(pool + base + koff, Ks + j * 512);
+        lds_dma16(pool + base + voff, Vs + j * 512);
+      }
+    };
 
     floatx16 oacc[RT][4];
     float m_run[RT], l_run[RT];
@@ -132,166 +221,123 @@ k_decode_attn(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         for (int e = 0; e < 16; ++e) oacc[rt][mt][e] = 0.f;
     }
 
-    const int n_tiles = (nk + kTile - 1) / kTile;
-    uint4 rk[8], rv[4][2];
-    const int64_t koff = tile_off(g, layer, 0, gk, 0), voff = tile_off(g, layer, 1, gk, 0);
-    auto kaddr = [&](int kk, int64_t base) -> const uint16_t* {
-      return pool + (int64_t)tb[kk / g.B] * g.block_elems + base + (kk % g.B) * kDh;
-    };
-    auto gload = [&](int t) {
-      const int k0 = t * kTile;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int q = tid + 256 * i, r = q >> 4, cc = q & 15;
-        const int kk = k0 + r;
-        rk[i] = kk < nk ? *(const uint4*)(kaddr(kk, koff) + cc * 8) : make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = tid + 256 * i, kp = q & 63, cc = q >> 6;
-        const int kk = k0 + 2 * kp;
-        rv[i][0] = kk < nk ? *(const uint4*)(kaddr(kk, voff) + cc * 8) : make_uint4(0, 0, 0, 0);
-        rv[i][1] = kk + 1 < nk ? *(const uint4*)(kaddr(kk + 1, voff) + cc * 8)
-                               : make_uint4(0, 0, 0, 0);
-      }
-    };
-    auto sstore = [&]() {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int q = tid + 256 * i, r = q >> 4, cc = q & 15;
-        *(uint4*)(sK + r * kLd + cc * 8) = rk[i];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = tid + 256 * i, kp = q & 63, cc = q >> 6;
-        const uint32_t* a0 = (const uint32_t*)&rv[i][0];
-        const uint32_t* a1 = (const uint32_t*)&rv[i][1];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t lo = (e & 1) ? (a0[e >> 1] >> 16) : (a0[e >> 1] & 0xffffu);
-          const uint32_t hi = (e & 1) ? (a1[e >> 1] >> 16) : (a1[e >> 1] & 0xffffu);
-          *(uint32_t*)(sV + (cc * 8 + e) * kVLd + 2 * kp) = lo | (hi << 16);
-        }
-      }
-    };
-
+    const int n_tiles = (nk + kKT - 1) / kKT;
+    for (int st = 0; st < S - 1 && st < n_tiles; ++st) issue(st, st);
     for (int t = 0; t < n_tiles; ++t) {
-      gload(t);         // two workgroups per CU hide each other's load latency
-      __syncthreads();  // previous tile fully consumed
-      sstore();
-      __syncthreads();
-      const int kw = wave * 32;  // this wave's keys within the tile
+      // copies of this wave complete in order: stage t is ready once at most
+      // the stages issued after it are pending (2 * kKT / 4 copies each)
+      const int ahead = min(S - 2, n_tiles - 1 - t);
+      if (ahead >= 2)
+        wait_vmcnt<4 * kKT / 4>();
+      else if (ahead == 1)
+        wait_vmcnt<2 * kKT / 4>();
+      else
+        wait_vmcnt<0>();
+      // stage (t - 1) % S was consumed in the previous iteration
+      if (t + S - 1 < n_tiles) issue(t + S - 1, (t + S - 1) % S);
+      const uint16_t* Ks = smem + (t % S) * kStage;
+      const uint16_t* Vs = Ks + kKT * kDh;
+      const int k0 = t * kKT;
+
+      floatx16 sacc[RT];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[rt][e] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 kf = *(const bf16x8*)(Ks + col * kDh + (((ks * 2 + hl) ^ (col & 15)) * 8));
+        sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], sacc[0], 0, 0, 0);
+        if (two)
+          sacc[RT - 1] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[RT - 1][ks], sacc[RT - 1], 0, 0, 0);
+      }
+      const bool tail = k0 + kKT > nk;  // wave-uniform
+      bf16x8 pf[RT][2];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        floatx16 sacc;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          const bf16x8 kf = *(const bf16x8*)(sK + (kw + col) * kLd + ks * 16 + hl * 8);
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[rt][ks], sacc, 0, 0, 0);
-        }
+        if (rt > 0 && !two) break;
         float mx = -INFINITY;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int kk = t * kTile + kw + (e >> 2) * 8 + hl * 4 + (e & 3);
-          float sv = sacc[e] * qk_scale_log2;
-          if (kk >= nk) sv = -INFINITY;
-          sacc[e] = sv;
+          float sv = sacc[rt][e];
+          if (tail) {
+            const int kk = k0 + (e >> 2) * 8 + hl * 4 + (e & 3);
+            if (kk >= nk) sv = -INFINITY;
+          }
+          sacc[rt][e] = sv;
           mx = fmaxf(mx, sv);
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[rt], mx);
+        mx = fmaxf(mx, __shfl_xor(mx, 32)) * qk_scale_log2;
+        const float m_new = mx > m_run[rt] + 8.f ? mx : m_run[rt];
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run[rt] - m_use);
-        float ps = 0.f;
-        bf16x8 pf[2];
+        const bool moved =
+            __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run[rt]) != 0)) != 0;
+        float psum = 0.f;
 #pragma unroll
         for (int hs = 0; hs < 2; ++hs) {
           float p[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            p[j] = exp2f(sacc[hs * 8 + j] - m_use);
-            ps += p[j];
+            p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[rt][hs * 8 + j], qk_scale_log2, -m_use));
+            psum += p[j];
           }
-          uint32_t wds[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
-                             pack2(p[6], p[7])};
-          pf[hs] = __builtin_bit_cast(bf16x8, *(uint4*)wds);
+          uint32_t wv[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
+                            pack2(p[6], p[7])};
+          pf[rt][hs] = __builtin_bit_cast(bf16x8, *(uint4*)wv);
         }
-        l_run[rt] = l_run[rt] * alpha + ps;
+        if (moved) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[rt] - m_use);
+          l_run[rt] *= alpha;
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) oacc[rt][mt][e] *= alpha;
+        }
+        l_run[rt] += psum;
         m_run[rt] = m_new;
+      }
+      // O^T += V^T P^T, V^T operands by transposed LDS reads
+      const int g4 = lane >> 4, li = lane & 15;
+#pragma unroll
+      for (int s4 = 0; s4 < 2; ++s4) {
+        const int key_a = s4 * 16 + (g4 >> 1) * 4 + (li >> 2), key_b = key_a + 8;
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) oacc[rt][mt][e] *= alpha;
-#pragma unroll
-          for (int hs = 0; hs < 2; ++hs) {
-            const uint16_t* vp = sV + (mt * 32 + col) * kVLd + kw + hs * 16 + hl * 4;
-            const uint2 v0 = *(const uint2*)vp;
-            const uint2 v1 = *(const uint2*)(vp + 8);
-            const uint4 vv = make_uint4(v0.x, v0.y, v1.x, v1.y);
-            oacc[rt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, vv), pf[hs], oacc[rt][mt], 0, 0, 0);
-          }
+          const int dc = mt * 32 + (g4 & 1) * 16 + (li & 3) * 4;
+          const int ch = dc >> 3, hf = dc & 7;
+          const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              KV_LDS4(Vs + key_a * kDh + ((ch ^ (key_a & 15)) * 8) + hf));
+          const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              KV_LDS4(Vs + key_b * kDh + ((ch ^ (key_b & 15)) * 8) + hf));
+          const v4s vv[2] = {r0, r1};
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+          oacc[0][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[0][s4], oacc[0][mt], 0, 0, 0);
+          if (two)
+            oacc[RT - 1][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[RT - 1][s4],
+                                                                       oacc[RT - 1][mt], 0, 0, 0);
         }
       }
     }
 
-    // ---- combine the four wavefronts per query vector, write partials
-    float* so = (float*)smem;             // [4 waves][32 vectors][128]
-    float* sm = so + 4 * 32 * kDh;        // [4 waves][32] m, then [4][32] l
-    static_assert(4 * 32 * kDh * 4 + 2 * 4 * 32 * 4 <= kKBytes + kVBytes, "combine scratch");
+    // partials of this unit's query vectors for chunk c
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      __syncthreads();  // LDS tiles (or the previous round) no longer read
       const float lt = l_run[rt] + __shfl_xor(l_run[rt], 32);
-      if (hl == 0) {
-        sm[wave * 32 + col] = m_run[rt];
-        sm[128 + wave * 32 + col] = lt;
-      }
+      if (qrow[rt] < 0) continue;
+      float* pp = part + ((((int64_t)lc * b + qrow[rt]) * g.Hq + qhead[rt]) * n_chunks + c) * kPart;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int dc = mt * 32 + q * 8 + hl * 4;
-          *(float4*)(so + (wave * 32 + col) * kDh + dc) =
+        for (int q = 0; q < 4; ++q)
+          *(float4*)(pp + 4 + mt * 32 + q * 8 + hl * 4) =
               make_float4(oacc[rt][mt][q * 4], oacc[rt][mt][q * 4 + 1], oacc[rt][mt][q * 4 + 2],
                           oacc[rt][mt][q * 4 + 3]);
-        }
-      __syncthreads();
-      for (int i = tid; i < 32 * (kDh / 4); i += 256) {
-        const int r = i / (kDh / 4), d4 = (i % (kDh / 4)) * 4;
-        const int rr = rt * 32 + r;
-        if (rr >= R) continue;
-        float mw[4], m2 = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          mw[w] = sm[w * 32 + r];
-          m2 = fmaxf(m2, mw[w]);
-        }
-        const float mu = m2 == -INFINITY ? 0.f : m2;
-        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        float l2 = 0.f;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float sc = exp2f(mw[w] - mu);
-          const float4 v = *(const float4*)(so + (w * 32 + r) * kDh + d4);
-          acc4.x += v.x * sc;
-          acc4.y += v.y * sc;
-          acc4.z += v.z * sc;
-          acc4.w += v.w * sc;
-          l2 += sm[128 + w * 32 + r] * sc;
-        }
-        const int sq = s_mem[rr / G], h = gk * G + rr % G;
-        float* pp = part + ((((int64_t)lc * b + sq) * g.Hq + h) * n_chunks + c) * kPart;
-        *(float4*)(pp + 4 + d4) = acc4;
-        if (d4 == 0) {
-          pp[0] = m2;
-          pp[1] = l2;
-        }
+      if (hl == 0) {
+        pp[0] = m_run[rt];
+        pp[1] = lt;
       }
     }
-    __syncthreads();  // partial writes done with the LDS before the next group
   }
 }
 
@@ -326,27 +372,50 @@ int decode_chunks(const AppendDesc& a) { return (a.max_keys + kCK - 1) / kCK; }
 
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
   const int G = g.Hq / g.Hkv;
+  // kCK % B == 0 makes B a power of two with at most 64 block ids per chunk
   return dtype == KV_DTYPE_BF16 && g.dh == kDh && a.T == 1 && a.batch * G <= 64 &&
-         kCK % g.B == 0 && g.B >= 16;
+         kCK % g.B == 0 && g.B >= 16 && g.b_shift >= 0;
 }
 
+namespace {
+size_t part_bytes(const PoolGeom& g, const AppendDesc& a) {
+  return ((size_t)g.L * a.batch * g.Hq * decode_chunks(a) * kPart * sizeof(float) + 255) & ~size_t(255);
+}
+size_t unit_bytes(const AppendDesc& a) {
+  return ((size_t)decode_chunks(a) * a.batch * sizeof(DecodeUnit) + 255) & ~size_t(255);
+}
+}  // namespace
+
 size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a) {
-  return (size_t)g.L * a.batch * g.Hq * decode_chunks(a) * kPart * sizeof(float);
+  return part_bytes(g, a) + unit_bytes(a) + (((size_t)decode_chunks(a) * sizeof(int) + 255) & ~size_t(255));
+}
+
+size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_keys) {
+  const int64_t chunks = (max_keys + kCK - 1) / kCK;
+  return (size_t)L * batch * Hq * chunks * kPart * sizeof(float) +
+         (size_t)chunks * batch * sizeof(DecodeUnit) + (size_t)chunks * sizeof(int) + 3 * 256;
 }
 
 hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
-                              void* part, int lc, int l0, hipStream_t s) {
+                              void* scratch, int lc, int l0, hipStream_t s) {
   const int G = g.Hq / g.Hkv;
   const int nch = decode_chunks(a);
+  float* part = (float*)scratch;
+  DecodeUnit* units = (DecodeUnit*)((char*)scratch + part_bytes(g, a));
+  int* n_units = (int*)((char*)units + unit_bytes(a));
+  if (l0 == 0) {  // the grouping holds for every layer group of the call
+    const size_t dyn = (size_t)a.batch * (kCK / g.B) * sizeof(int);
+    k_decode_plan<<<nch, 64, dyn, s>>>(g, a, units, n_units);
+  }
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
-  dim3 grid(nch, g.Hkv, lc);
-  const size_t dyn = (size_t)a.batch * (kCK / g.B) * sizeof(int);
+  const int slots = std::min(nch * a.batch, 2 * nch + a.batch);
+  dim3 grid(slots, g.Hkv, lc);
   if (a.batch * G <= 32)
-    k_decode_attn<1><<<grid, 256, dyn, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0,
-                                            sc);
+    k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+                                              nch, l0, sc);
   else
-    k_decode_attn<2><<<grid, 256, dyn, s>>>(g, (const uint16_t*)qbuf, a, (float*)part, nch, l0,
-                                            sc);
+    k_decode_stream<2, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+                                              nch, l0, sc);
   return hipGetLastError();
 }
 

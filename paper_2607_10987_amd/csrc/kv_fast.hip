@@ -6,6 +6,7 @@ namespace kvs {
 int decode_chunks(const AppendDesc& a);
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a);
 size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a);
+size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_keys);
 hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
                               void* part, int lc, int l0, hipStream_t s);
 hipError_t launch_decode_merge(const PoolGeom& g, const AppendDesc& a, void* o, const void* part,
@@ -16,9 +17,8 @@ size_t fast_scratch_bytes(const PoolGeom& g, int dtype, const AppendDesc& a) {
 }
 
 size_t fast_scratch_bound(const kv_model_cfg& c, int64_t, int32_t batch, int64_t max_keys) {
-  // split-key partials of a decode call: L x batch x Hq x chunks x (4 + dh) floats
-  const int64_t chunks = (max_keys + 1023) / 1024;
-  return (size_t)c.n_layers * batch * c.n_q_heads * chunks * (c.head_dim + 4) * sizeof(float);
+  // split-key partials and the work-unit plan of a decode call
+  return decode_scratch_bound(c.n_layers, batch, c.n_q_heads, max_keys);
 }
 
 bool qkv_mfma_ok(const PoolGeom& g, int dtype);
