@@ -152,19 +152,26 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
     total += v;
   }
+  total = __builtin_amdgcn_readfirstlane(total);
+  const uint32_t lds0 = lds_addr(smem);
+  const int64_t kv_gap = (voff - koff) * 2;  // bytes from a K row to its V row
 
   for (int u = blockIdx.x; u < total; u += gridDim.x) {
     int c, gi;
     locate_unit(n_units, n_chunks, u, &c, &gi);
-    const DecodeUnit un = units[c * b + gi];
-    const int nk = un.nk;
-    const uint64_t mask = ((uint64_t)un.mask_hi << 32) | un.mask_lo;
+    c = __builtin_amdgcn_readfirstlane(c);
+    gi = __builtin_amdgcn_readfirstlane(gi);
+    const DecodeUnit* up = units + c * b + gi;
+    const int nk = __builtin_amdgcn_readfirstlane(up->nk);
+    const int lead = __builtin_amdgcn_readfirstlane(up->lead);
+    const uint64_t mask = ((uint64_t)__builtin_amdgcn_readfirstlane(up->mask_hi) << 32) |
+                          (uint32_t)__builtin_amdgcn_readfirstlane(up->mask_lo);
     const int R = __popcll(mask) * G;  // query vectors of the unit
     const bool two = RT > 1 && R > 32;
     const int c0 = c * kCK;
-    // lane j: block id of the leader's entry j of the chunk
+    // lane j: block id of the leader's entry j of the chunk (0 past the end)
     const int tbl = (lane << g.b_shift) < nk
-                        ? g.tables[(int64_t)a.seq[un.lead].slot * g.max_blocks +
+                        ? g.tables[(int64_t)a.seq[lead].slot * g.max_blocks +
                                    (c0 >> g.b_shift) + lane]
                         : 0;
 
@@ -192,20 +199,22 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) settle(qf[rt][ks]);
 
-    // stage loads: 8 copies of 1 KiB (4 key rows) per operand; rows past the
-    // unit's last key repeat that key, whose score is masked
+    // stage loads: 8 copies of 1 KiB (4 key rows, all in one block since
+    // B >= 16) per operand, block base in scalar registers.  Rows past the
+    // unit's last key read slots of a real block; their scores are masked and
+    // their V rows zeroed in LDS before use.
     auto issue = [&](int tile, int buf) {
-      uint16_t* Ks = smem + buf * kStage;
-      uint16_t* Vs = Ks + kKT * kDh;
+      const uint32_t ks_lds = lds0 + buf * kStage * 2;
 #pragma unroll
       for (int j = 0; j < kKT / 4; ++j) {
+        const int key0 = tile * kKT + j * 4;
+        const int id = __builtin_amdgcn_readlane(tb, key0 >> g.b_shift);
+        const char* kb = (const char*)pool +
+                         ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
         const int r = j * 4 + (lane >> 4);
-        const int cc = (lane & 15) ^ (r & 15);
-        const int key = min(tile * kKT + r, nk - 1);
-        const int id = __shfl(tb, key >> g.b_shift);
-        const int64_t base = (int64_t)id * g.block_elems + (key & (g.B - 1)) * kDh + cc * 8;
-        lds_dma16(pool + base + koff, Ks + j * 512);
-        lds_dma16(pool + base + voff, Vs + j * 512);
+        const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ (r & 15)) * 16);
+        lds_dma16_sv(kb, vo, ks_lds + j * 1024);
+        lds_dma16_sv(kb + kv_gap, vo, ks_lds + kKT * kDh * 2 + j * 1024);
       }
     };
 
@@ -238,6 +247,12 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       const uint16_t* Ks = smem + (t % S) * kStage;
       const uint16_t* Vs = Ks + kKT * kDh;
       const int k0 = t * kKT;
+      const bool tail = k0 + kKT > nk;  // wave-uniform
+      if (tail) {  // V rows of keys >= nk may hold anything: zero them
+        uint16_t* Vw = (uint16_t*)Vs;
+        for (int i = (nk - k0) * (kDh / 8) + lane; i < kKT * (kDh / 8); i += 64)
+          *(uint4*)(Vw + i * 8) = make_uint4(0, 0, 0, 0);
+      }
 
       floatx16 sacc[RT];
 #pragma unroll
@@ -252,7 +267,6 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
           sacc[RT - 1] =
               __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[RT - 1][ks], sacc[RT - 1], 0, 0, 0);
       }
-      const bool tail = k0 + kKT > nk;  // wave-uniform
       bf16x8 pf[RT][2];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
@@ -341,29 +355,58 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   }
 }
 
-// grid (batch * Hq, lc), block 128: combine the chunk partials of one query.
-__global__ void __launch_bounds__(128)
+// grid (batch * Hq, lc), block 64: combine the chunk partials of one query.
+// Lane i owns output channels 2i, 2i + 1; the chunk weights exp2(m_c - max)
+// are computed once per chunk and broadcast through LDS.
+__global__ void __launch_bounds__(64)
 k_decode_merge(PoolGeom g, AppendDesc a, const float* __restrict__ part, int n_chunks,
                uint16_t* __restrict__ o, int l0) {
-  const int sh = blockIdx.x, lc = blockIdx.y;
+  __shared__ float s_w[64];
+  const int sh = blockIdx.x, lc = blockIdx.y, lane = threadIdx.x;
   const int s = sh / g.Hq, h = sh % g.Hq;
   const int b = a.batch;
   const int n = a.seq[s].n_before + 1;
   const int nc = (n + kCK - 1) / kCK;
   const float* pp = part + (((int64_t)lc * b + s) * g.Hq + h) * n_chunks * kPart;
   float mx = -INFINITY;
-  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, pp[c * kPart]);
-  float lsum = 0.f, acc = 0.f;
-  const int dc = threadIdx.x;
-  for (int c = 0; c < nc; ++c) {
-    const float wgt = exp2f(pp[c * kPart] - mx);
-    lsum += pp[c * kPart + 1] * wgt;
-    acc += pp[c * kPart + 4 + dc] * wgt;
+  for (int c = lane; c < nc; c += 64) mx = fmaxf(mx, pp[(int64_t)c * kPart]);
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
+  float lsum = 0.f;
+  float2 acc = make_float2(0.f, 0.f);
+  for (int c0 = 0; c0 < nc; c0 += 64) {
+    const int c = c0 + lane;
+    float w = 0.f;
+    if (c < nc) {
+      w = exp2f(pp[(int64_t)c * kPart] - mx);
+      lsum += pp[(int64_t)c * kPart + 1] * w;
+    }
+    s_w[lane] = w;
+    __syncthreads();
+    const int cn = min(64, nc - c0);
+    const float* q = pp + (int64_t)c0 * kPart + 4 + 2 * lane;
+    int i = 0;
+    for (; i + 4 <= cn; i += 4) {
+      const float2 v0 = *(const float2*)(q + (int64_t)i * kPart);
+      const float2 v1 = *(const float2*)(q + (int64_t)(i + 1) * kPart);
+      const float2 v2 = *(const float2*)(q + (int64_t)(i + 2) * kPart);
+      const float2 v3 = *(const float2*)(q + (int64_t)(i + 3) * kPart);
+      acc.x += v0.x * s_w[i] + v1.x * s_w[i + 1] + v2.x * s_w[i + 2] + v3.x * s_w[i + 3];
+      acc.y += v0.y * s_w[i] + v1.y * s_w[i + 1] + v2.y * s_w[i + 2] + v3.y * s_w[i + 3];
+    }
+    for (; i < cn; ++i) {
+      const float2 v = *(const float2*)(q + (int64_t)i * kPart);
+      acc.x += v.x * s_w[i];
+      acc.y += v.y * s_w[i];
+    }
+    __syncthreads();
   }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) lsum += __shfl_xor(lsum, d);
+  const float inv = 1.f / lsum;
   const int l = l0 + lc;
-  const float v = acc / lsum;
-  const __bf16 bv = (__bf16)v;
-  o[(((int64_t)l * b + s) * g.Hq + h) * kDh + dc] = __builtin_bit_cast(uint16_t, bv);
+  *(uint32_t*)(o + (((int64_t)l * b + s) * g.Hq + h) * kDh + 2 * lane) =
+      pack2(acc.x * inv, acc.y * inv);
 }
 
 }  // namespace
@@ -411,10 +454,10 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   const int slots = std::min(nch * a.batch, 2 * nch + a.batch);
   dim3 grid(slots, g.Hkv, lc);
   if (a.batch * G <= 32)
-    k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+    k_decode_stream<1, 2><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, l0, sc);
   else
-    k_decode_stream<2, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+    k_decode_stream<2, 2><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, l0, sc);
   return hipGetLastError();
 }
@@ -422,7 +465,7 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
 hipError_t launch_decode_merge(const PoolGeom& g, const AppendDesc& a, void* o, const void* part,
                                int l0, int lc, hipStream_t s) {
   dim3 grid(a.batch * g.Hq, lc);
-  k_decode_merge<<<grid, 128, 0, s>>>(g, a, (const float*)part, decode_chunks(a), (uint16_t*)o,
+  k_decode_merge<<<grid, 64, 0, s>>>(g, a, (const float*)part, decode_chunks(a), (uint16_t*)o,
                                       l0);
   return hipGetLastError();
 }

@@ -31,6 +31,22 @@ __device__ inline void lds_dma16(const void* gptr, void* lds) {
                : "memory", "m0");
 }
 
+// LDS byte address of a __shared__ pointer, wave-uniform.
+__device__ inline uint32_t lds_addr(const void* lds) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds);
+}
+
+// The same copy with the global address split into a wave-uniform base
+// (scalar registers) and a per-lane 32-bit byte offset; `lds` is an LDS byte
+// address from lds_addr().
+__device__ inline void lds_dma16_sv(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
 template <int N>
 __device__ inline void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
