@@ -1,12 +1,12 @@
-// Causal grouped-query attention over the paged cache on MFMA (bf16 inputs,
-// fp32 softmax and accumulation), head_dim 128.
+// Causal grouped-query attention of an append (prefill) over the paged cache
+// on MFMA: bf16 inputs, fp32 softmax and accumulation, head_dim 128.
 //
-// One workgroup = one sequence's tile of 32 query tokens x one KV head x one
-// layer; wavefront w handles query head g * G + w, so the G heads that share
-// a KV head share every K / V tile staged in LDS.  Keys are walked in tiles of
-// 64 (4 paged blocks of 16, or 2 of 32), looked up through the block table.
+// One workgroup = 8 wavefronts = the G query heads of one KV head x (8 / G)
+// groups of 32 query tokens of one sequence, in one layer; all eight share
+// every K / V tile of 64 keys staged in LDS.  Keys are looked up through the
+// block table (its slice for this workgroup is staged in LDS once).
 //
-// Both products keep the query token in the MFMA "column" so that every
+// Both products keep the query token in the MFMA column so that every
 // per-token quantity is lane-local:
 //   S^T [64 keys x 32 tok] = K [keys x dh] . Q^T      (A: K rows from LDS,
 //                                                     B: Q rows, registers)
@@ -16,10 +16,29 @@
 // {8q + 4h + r : q < 4, r < 4} of its token (h = lane / 32).  Taking the PV
 // contraction over keys in the order (4h + r, 8 + 4h + r) for each group of
 // 16 keys makes those registers exactly the B operand, so P never leaves the
-// lane; V^T is staged in LDS (transposed on the way in) and read with the
-// same key order.  Softmax: running max / running sum per token in base 2
-// (scores pre-multiplied by log2(e) / sqrt(dh)), halves of a token combined
-// with one lane swap.
+// lane.  Softmax: running max / running sum per token in base 2 (scores
+// scaled by log2(e) / sqrt(dh)); the max is only moved when it grows by more
+// than 8 (a factor 2^8), so the accumulator rescale is rare.
+//
+// Staging: K and V tiles stream straight from the pool into LDS
+// (global_load_lds_dwordx4) through 4 stages, unpadded 256-byte key rows with
+// the 16-byte chunk c of row r stored at slot c ^ (r & 15), so that 16
+// consecutive rows read at one chunk hit distinct bank groups.  V stays key
+// major; its operand (4 consecutive keys of one channel per half) is read
+// with ds_read_b64_tr_b16: within each group of 16 lanes, lane i addressing
+// row key0 + i / 4, channels c0 + 4 (i % 4) .. + 3 receives keys
+// key0 .. key0 + 3 of channel c0 + i.
+//
+// Software pipeline: iteration t issues the QK^T products of tile t + 1
+// before the softmax of tile t, so that the matrix cores work on the next
+// scores while the vector ALUs exponentiate the current ones; then the PV
+// products of tile t.
+//
+// Workgroup order: consecutive workgroups are dispatched round-robin to the
+// 8 XCDs, each with its own L2.  The linear workgroup id is permuted so that
+// each XCD receives a contiguous range of (layer, KV head, query tile)
+// triples: the query tiles of one (layer, KV head) read its K / V through
+// one L2.
 #include "kv_dma.h"
 #include "kv_fast.h"
 
@@ -28,233 +47,35 @@ namespace kvs {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
-
-constexpr int kDh = 128;
-constexpr int kQT = 32;            // query tokens per workgroup
-constexpr int kKT = 64;            // keys per tile
-constexpr int kKLd = kDh + 8;      // K tile row stride (elements)
-constexpr int kVLd = kKT + 8;      // V^T tile row stride (elements)
-constexpr int kStage = kKT * kKLd + kDh * kVLd;
-
-__device__ inline uint32_t pack2(float a, float b) {
-  const __bf16 x = (__bf16)a, y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
-}
-
-template <int G>
-__global__ void __launch_bounds__(64 * G, 8 / G)
-k_attn_prefill(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
-               uint16_t* __restrict__ o, int l0, float qk_scale_log2) {
-  constexpr int NT = 64 * G;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int hl = lane >> 5;       // lane half
-  const int col = lane & 31;      // token within the tile
-  const int qt_per_seq = (a.T + kQT - 1) / kQT;
-  const int seq = blockIdx.x / qt_per_seq;
-  const int qt = qt_per_seq - 1 - (blockIdx.x % qt_per_seq);  // long tiles first
-  const int gk = blockIdx.y;
-  const int lc = blockIdx.z, l = l0 + lc;
-  const int M = a.batch * a.T;
-  const SeqDesc sd = a.seq[seq];
-  const int n_keys = sd.n_before + a.T;
-  const int t0 = qt * kQT;
-  const int tq = t0 + col;                      // this lane's query token
-  const int uq = sd.n_before + tq;              // its key index (causal limit)
-  const bool q_valid = tq < a.T;
-  const int key_end = min(n_keys, sd.n_before + t0 + kQT);  // keys this tile can see
-  const int n_tiles = (key_end + kKT - 1) / kKT;
-  const int h = gk * G + wave;
-  const int32_t* trow = g.tables + (int64_t)sd.slot * g.max_blocks;
-  const uint16_t* pool = (const uint16_t*)g.pool;
-
-  // Q^T operand: token col, dh chunk (ks * 16 + hl * 8 .. + 8), 8 k-steps
-  bf16x8 qf[8];
-  {
-    const int row = seq * a.T + min(tq, a.T - 1);
-    const uint16_t* qp = qbuf + (((int64_t)lc * M + row) * g.Hq + h) * kDh;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks) qf[ks] = *(const bf16x8*)(qp + ks * 16 + hl * 8);
-  }
-
-  // tile loaders: K rows [64][128] and V transposed [128][64]
-  constexpr int KCH = kKT * kDh / 8 / NT;        // 16-byte K chunks per thread
-  constexpr int VIT = (kKT / 2) * (kDh / 8) / NT; // V items (key pair, 8 channels) per thread
-  uint4 rk[KCH], rv[VIT][2];
-  auto key_addr = [&](int kk, int kv) -> const uint16_t* {
-    const int32_t blk = trow[kk / g.B];
-    return pool + (int64_t)blk * g.block_elems + tile_off(g, l, kv, gk, kk % g.B);
-  };
-  auto gload = [&](int tile) {
-    const int k0 = tile * kKT;
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int q = tid + NT * i, r = q >> 4, c = q & 15;
-      const int kk = k0 + r;
-      rk[i] = kk < n_keys ? *(const uint4*)(key_addr(kk, 0) + c * 8) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < VIT; ++i) {
-      const int q = tid + NT * i, kp = q & 31, c = q >> 5;
-      const int kk = k0 + 2 * kp;
-      rv[i][0] = kk < n_keys ? *(const uint4*)(key_addr(kk, 1) + c * 8) : make_uint4(0, 0, 0, 0);
-      rv[i][1] = kk + 1 < n_keys ? *(const uint4*)(key_addr(kk + 1, 1) + c * 8)
-                                 : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-    uint16_t* Ks = smem + buf * kStage;
-    uint16_t* Vt = Ks + kKT * kKLd;
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int q = tid + NT * i, r = q >> 4, c = q & 15;
-      *(uint4*)(Ks + r * kKLd + c * 8) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VIT; ++i) {
-      const int q = tid + NT * i, kp = q & 31, c = q >> 5;
-      const uint32_t* a0 = (const uint32_t*)&rv[i][0];
-      const uint32_t* a1 = (const uint32_t*)&rv[i][1];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t lo = (e & 1) ? (a0[e >> 1] >> 16) : (a0[e >> 1] & 0xffffu);
-        const uint32_t hi = (e & 1) ? (a1[e >> 1] >> 16) : (a1[e >> 1] & 0xffffu);
-        *(uint32_t*)(Vt + (c * 8 + e) * kVLd + 2 * kp) = lo | (hi << 16);
-      }
-    }
-  };
-
-  floatx16 oacc[4];
-#pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) oacc[mt][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const int cur = tile & 1;
-    if (tile + 1 < n_tiles) gload(tile + 1);
-    const uint16_t* Ks = smem + cur * kStage;
-    const uint16_t* Vt = Ks + kKT * kKLd;
-    const int k0 = tile * kKT;
-
-    // S^T = K Q^T for two 32-key halves of the tile
-    floatx16 sacc[2];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[kt][e] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(Ks + (kt * 32 + col) * kKLd + ks * 16 + hl * 8);
-        sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
-      }
-    }
-    // mask, running max on raw scores (scale > 0 commutes with max)
-    const bool need_mask = k0 + kKT - 1 > sd.n_before + t0 || k0 + kKT > n_keys || !q_valid;
-    float mt_max = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float s = sacc[kt][e];
-        if (need_mask) {
-          const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
-          if (kk > uq || kk >= n_keys) s = -INFINITY;
-        }
-        sacc[kt][e] = s;
-        mt_max = fmaxf(mt_max, s);
-      }
-    mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32)) * qk_scale_log2;
-    // Lazy rescaling: the running max only moves when a score exceeds it by
-    // more than 2^8 in the exponent; until then p <= 256, exact in fp32 and
-    // representable in bf16, and O is not rescaled (the final division by l
-    // uses the same reference, so the result is unchanged).
-    const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;  // fully masked (padding) rows
-    const bool moved = __ballot(m_new != m_run) != 0;
-    float psum = 0.f;
-    bf16x8 pf[4];  // B operands of the PV product, one per 16-key step
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int hs = 0; hs < 2; ++hs) {
-        float p[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          p[j] = exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
-          psum += p[j];
-        }
-        uint32_t w[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
-                         pack2(p[6], p[7])};
-        pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(uint4*)w);
-      }
-    if (moved) {
-      const float alpha = exp2f(m_run - m_use);
-      l_run *= alpha;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
-    }
-    l_run += psum;
-    m_run = m_new;
-    // O^T += V^T P^T; 16-key step s covers keys 16 s + {4h + r, 8 + 4h + r}
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const uint16_t* vp = Vt + (mt * 32 + col) * kVLd + s4 * 16 + hl * 4;
-        const uint2 v0 = *(const uint2*)vp;
-        const uint2 v1 = *(const uint2*)(vp + 8);
-        const uint4 vv = make_uint4(v0.x, v0.y, v1.x, v1.y);
-        oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf[s4],
-                                                           oacc[mt], 0, 0, 0);
-      }
-    }
-    if (tile + 1 < n_tiles) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  // normalise and store: lane holds channels 32 mt + 8 q + 4 h + r of its token
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!q_valid) return;
-  const float inv = 1.f / l_tot;
-  const int row = seq * a.T + tq;
-  uint16_t* op = o + (((int64_t)l * M + row) * g.Hq + h) * kDh;
-#pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int c0 = mt * 32 + q * 8 + hl * 4;
-      *(uint2*)(op + c0) = make_uint2(pack2(oacc[mt][q * 4] * inv, oacc[mt][q * 4 + 1] * inv),
-                                      pack2(oacc[mt][q * 4 + 2] * inv, oacc[mt][q * 4 + 3] * inv));
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Pipelined variant: K and V tiles stream straight from the paged pool into
-// LDS (global_load_lds_dwordx4, three tiles in flight), unpadded 256-byte key
-// rows with the 16-byte chunk c of row r stored at slot c ^ (r & 15), so that
-// 16 consecutive rows read at one chunk hit 16 distinct bank groups.  V stays
-// in key-major order; its MFMA operand (4 consecutive keys of one channel per
-// half) is read with ds_read_b64_tr_b16: within each group of 16 lanes, lane
-// i addressing row key0 + i / 4, channels c0 + 4 (i % 4) .. + 3 receives the
-// 4 keys key0 .. key0 + 3 of channel c0 + i.  Eight wavefronts: G query heads
-// x (8 / G) groups of 32 query tokens share every staged tile.  The block
-// table slice the workgroup needs is staged in LDS once.
-constexpr int kPW = 8;                 // wavefronts per workgroup
-constexpr int kPS = 3;                 // pipeline stages
-constexpr int kPTile = kKT * kDh;      // elements of one K (or V) tile
-
 typedef short v4s __attribute__((ext_vector_type(4)));
 #define KV_LDS4(p) ((__attribute__((address_space(3))) v4s*)(p))
 
+constexpr int kDh = 128;
+constexpr int kKT = 64;             // keys per tile
+constexpr int kPW = 8;              // wavefronts per workgroup
+constexpr int kPS = 4;              // pipeline stages
+constexpr int kPTile = kKT * kDh;   // elements of one K (or V) tile
+constexpr int kXcd = 8;             // XCDs per device
+constexpr size_t kLdsMax = 160 * 1024;
+constexpr size_t kStaticLds = (size_t)kPS * 2 * kPTile * 2;
+
+__device__ inline uint32_t cvt2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2){a, b}, bf16x2));
+}
+
+// Bijection of [0, n) that gives XCD x (= id % kXcd) a contiguous logical
+// range.
+__device__ inline int xcd_remap(int id, int n) {
+  const int per = (n + kXcd - 1) / kXcd;
+  const int tall = n % kXcd == 0 ? kXcd : n % kXcd;
+  const int x = id % kXcd, i = id / kXcd;
+  return x < tall ? x * per + i : tall * per + (x - tall) * (per - 1) + i;
+}
+
+// grid (batch x query tiles x Hkv x lc, flattened), block 512.
 template <int G>
 __global__ void __launch_bounds__(64 * kPW, 1)
 k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
@@ -263,14 +84,17 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   constexpr int QT = 32 * TG;       // query tokens per workgroup
   __shared__ __attribute__((aligned(16))) uint16_t smem[kPS * 2 * kPTile];
   extern __shared__ int s_tbl[];    // block ids of the keys this workgroup reads
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hl = lane >> 5, col = lane & 31;
   const int tg = wave / G, hw = wave % G;
   const int qt_per_seq = (a.T + QT - 1) / QT;
-  const int seq = blockIdx.x / qt_per_seq;
-  const int qt = qt_per_seq - 1 - (blockIdx.x % qt_per_seq);  // long tiles first
-  const int gk = blockIdx.y;
-  const int lc = blockIdx.z, l = l0 + lc;
+  const int nx = a.batch * qt_per_seq;
+  const int lid = xcd_remap(blockIdx.x, gridDim.x);
+  const int bx = lid % nx, gk = (lid / nx) % g.Hkv, lc = lid / (nx * g.Hkv);
+  const int seq = bx / qt_per_seq;
+  const int qt = qt_per_seq - 1 - (bx % qt_per_seq);  // long tiles first
+  const int l = l0 + lc;
   const int M = a.batch * a.T;
   const SeqDesc sd = a.seq[seq];
   const int n_keys = sd.n_before + a.T;
@@ -300,45 +124,47 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   }
   __syncthreads();  // s_tbl ready
 
-  // tile loads: 16 instructions of 1 KiB per operand (4 key rows each); wave w
-  // issues instructions w and w + 8 of K and of V
+  // Tile loads: 16 copies of 1 KiB (4 key rows of one block, as B >= 16) per
+  // operand; wave w issues copies w and w + 8 of K and of V.  Full tiles use a
+  // scalar block base; the last tile clamps rows past key_end to key_end - 1
+  // per lane (slots past the end of a state may hold anything).
   const int64_t koff = tile_off(g, l, 0, gk, 0), voff = tile_off(g, l, 1, gk, 0);
+  const int64_t kv_gap = (voff - koff) * 2;
+  const uint32_t lds0 = lds_addr(smem);
   auto issue = [&](int tile, int buf) {
-    uint16_t* Ks = smem + buf * 2 * kPTile;
-    uint16_t* Vs = Ks + kPTile;
+    if ((tile + 1) * kKT <= key_end) {
+      const uint32_t kl = lds0 + buf * 2 * kPTile * 2, vl = kl + kPTile * 2;
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int j = wave + jj * kPW;
-      const int r = j * 4 + (lane >> 4);
-      const int c = (lane & 15) ^ (r & 15);
-      const int key = min(tile * kKT + r, key_end - 1);  // rows past the end: any staged key
-      const int64_t base = (int64_t)s_tbl[key >> g.b_shift] * g.block_elems +
-                           (key & (g.B - 1)) * kDh + c * 8;
-      lds_dma16(pool + base + koff, Ks + j * 512);
-      lds_dma16(pool + base + voff, Vs + j * 512);
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = wave + jj * kPW;
+        const int key0 = tile * kKT + j * 4;
+        const int id = __builtin_amdgcn_readfirstlane(s_tbl[key0 >> g.b_shift]);
+        const char* kb = (const char*)pool +
+                         ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
+        const uint32_t vo =
+            (lane >> 4) * (kDh * 2) + (((lane & 15) ^ ((j * 4 + (lane >> 4)) & 15)) * 16);
+        lds_dma16_sv(kb, vo, kl + j * 1024);
+        lds_dma16_sv(kb + kv_gap, vo, vl + j * 1024);
+      }
+    } else {
+      uint16_t* Ks = smem + buf * 2 * kPTile;
+      uint16_t* Vs = Ks + kPTile;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = wave + jj * kPW;
+        const int r = j * 4 + (lane >> 4);
+        const int c = (lane & 15) ^ (r & 15);
+        const int key = min(tile * kKT + r, key_end - 1);
+        const int64_t base = (int64_t)s_tbl[key >> g.b_shift] * g.block_elems +
+                             (key & (g.B - 1)) * kDh + c * 8;
+        lds_dma16(pool + base + koff, Ks + j * 512);
+        lds_dma16(pool + base + voff, Vs + j * 512);
+      }
     }
   };
-
-  floatx16 oacc[4];
-#pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) oacc[mt][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    if (tile + 1 < n_tiles)
-      wait_vmcnt<4>();  // the next tile (4 copies per wave) may be pending
-    else
-      wait_vmcnt<0>();
-    lds_barrier();
-    if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
-    const uint16_t* Ks = smem + (tile % kPS) * 2 * kPTile;
-    const uint16_t* Vs = Ks + kPTile;
-    const int k0 = tile * kKT;
-
-    floatx16 sacc[2];
+  // S^T of one tile for this wave's 32 tokens
+  auto qk = [&](int buf, floatx16* sacc) {
+    const uint16_t* Ks = smem + buf * 2 * kPTile;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
@@ -350,27 +176,68 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
       }
     }
+  };
+
+  floatx16 oacc[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) oacc[mt][e] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // Copies of one wave complete in order, 4 per tile: tile t is ready once at
+  // most the 4 k copies of the k tiles issued after it are pending.
+  for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
+  if (n_tiles > 2)
+    wait_vmcnt<8>();
+  else if (n_tiles == 2)
+    wait_vmcnt<4>();
+  else
+    wait_vmcnt<0>();
+  lds_barrier();
+  floatx16 sacc[2];
+  qk(0, sacc);
+
+  for (int tile = 0; tile < n_tiles; ++tile) {
+    floatx16 snext[2];
+    if (tile + 1 < n_tiles) {
+      // tile + 1 ready, and every wave is done with tile - 1, whose buffer
+      // is refilled
+      if (tile + 2 < n_tiles)
+        wait_vmcnt<4>();
+      else
+        wait_vmcnt<0>();
+      lds_barrier();
+      if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
+      qk((tile + 1) % kPS, snext);
+    }
+    const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
+    const int k0 = tile * kKT;
+
     // wave-uniform: does any (query, key) pair of this tile need masking?
-    const bool need_mask = k0 + kKT - 1 > sd.n_before + t0 + tg * 32 || k0 + kKT > n_keys ||
-                           t0 + tg * 32 + 31 >= a.T;
+    const bool need_mask = __builtin_amdgcn_readfirstlane(
+                               (int)(k0 + kKT - 1 > sd.n_before + t0 + tg * 32 ||
+                                     k0 + kKT > n_keys || t0 + tg * 32 + 31 >= a.T)) != 0;
+    if (need_mask) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
+          if (kk > uq || kk >= n_keys) sacc[kt][e] = -INFINITY;
+        }
+    }
     float mt_max = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float sv = sacc[kt][e];
-        if (need_mask) {
-          const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
-          if (kk > uq || kk >= n_keys) sv = -INFINITY;
-        }
-        sacc[kt][e] = sv;
-        mt_max = fmaxf(mt_max, sv);
-      }
+      for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sacc[kt][e]);
     mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32)) * qk_scale_log2;
     const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     const bool moved = __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run) != 0)) != 0;
-    float psum = 0.f;
+    float ps0 = 0.f, ps1 = 0.f;
     bf16x8 pf[4];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -378,13 +245,16 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int hs = 0; hs < 2; ++hs) {
         float p[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < 8; ++j)
           p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
-          psum += p[j];
-        }
-        uint32_t wv[4] = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]),
-                          pack2(p[6], p[7])};
-        pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(uint4*)wv);
+        const uint32_t wv[4] = {cvt2(p[0], p[1]), cvt2(p[2], p[3]), cvt2(p[4], p[5]),
+                                cvt2(p[6], p[7])};
+        // row sum of the bf16 probabilities the PV product uses
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[0]), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[1]), ones, ps1, false);
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[2]), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[3]), ones, ps1, false);
+        pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(const uint4*)wv);
       }
     if (moved) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
@@ -394,7 +264,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
     }
-    l_run += psum;
+    l_run += ps0 + ps1;
     m_run = m_new;
     // O^T += V^T P^T, V^T operands by transposed LDS reads
     const int gi = lane >> 4, li = lane & 15;
@@ -415,6 +285,10 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                                                            oacc[mt], 0, 0, 0);
       }
     }
+    if (tile + 1 < n_tiles) {
+      sacc[0] = snext[0];
+      sacc[1] = snext[1];
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -427,42 +301,38 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int c0 = mt * 32 + q * 8 + hl * 4;
-      *(uint2*)(op + c0) = make_uint2(pack2(oacc[mt][q * 4] * inv, oacc[mt][q * 4 + 1] * inv),
-                                      pack2(oacc[mt][q * 4 + 2] * inv, oacc[mt][q * 4 + 3] * inv));
+      *(uint2*)(op + c0) = make_uint2(cvt2(oacc[mt][q * 4] * inv, oacc[mt][q * 4 + 1] * inv),
+                                      cvt2(oacc[mt][q * 4 + 2] * inv, oacc[mt][q * 4 + 3] * inv));
     }
+}
+
+size_t table_bytes(const PoolGeom& g, int max_keys) {
+  return (size_t)((max_keys + g.B - 1) / g.B) * sizeof(int);
 }
 
 }  // namespace
 
-bool attn_mfma_ok(const PoolGeom& g, int dtype) {
+bool attn_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
   const int G = g.Hq / g.Hkv;
-  return dtype == KV_DTYPE_BF16 && g.dh == kDh && (G == 4 || G == 8) && g.b_shift >= 0;
+  return dtype == KV_DTYPE_BF16 && g.dh == kDh && (G == 4 || G == 8) && g.b_shift >= 0 &&
+         g.B >= 16 && kStaticLds + table_bytes(g, a.max_keys) <= kLdsMax;
 }
 
 hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const AppendDesc& a, void* o,
                                int l0, int lc, hipStream_t s) {
   const int G = g.Hq / g.Hkv;
-  {
-    const int QT = 32 * (kPW / G);
-    const int qt = (a.T + QT - 1) / QT;
-    dim3 grid(a.batch * qt, g.Hkv, lc);
-    const float sc = 1.4426950408889634f / sqrtf((float)kDh);
-    const size_t dyn = (size_t)((a.max_keys + g.B - 1) / g.B) * sizeof(int);
-    if (G == 4)
-      k_attn_pipe<4><<<grid, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o, l0,
-                                                  sc);
-    else
-      k_attn_pipe<8><<<grid, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o, l0,
-                                                  sc);
-    return hipGetLastError();
-  }
-  const int qt = (a.T + kQT - 1) / kQT;
-  dim3 grid(a.batch * qt, g.Hkv, lc);
+  const int QT = 32 * (kPW / G);
+  const int qt = (a.T + QT - 1) / QT;
+  const int64_t n = (int64_t)a.batch * qt * g.Hkv * lc;
+  if (n > 0x7fffffff) return hipErrorInvalidValue;
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
+  const size_t dyn = table_bytes(g, a.max_keys);
   if (G == 4)
-    k_attn_prefill<4><<<grid, 256, 0, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o, l0, sc);
+    k_attn_pipe<4><<<(unsigned)n, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o,
+                                                     l0, sc);
   else
-    k_attn_prefill<8><<<grid, 512, 0, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o, l0, sc);
+    k_attn_pipe<8><<<(unsigned)n, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o,
+                                                     l0, sc);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ hipError_t launch_qkv_fast(const PoolGeom& g, int dtype, const void* x, const vo
   return launch_qkv_mfma(g, x, w, w_stride, a, qbuf, l0, lc, s);
 }
 
-bool attn_mfma_ok(const PoolGeom& g, int dtype);
+bool attn_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a);
 hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const AppendDesc& a, void* o,
                                int l0, int lc, hipStream_t s);
 
@@ -48,7 +48,7 @@ hipError_t launch_attn_fast(const PoolGeom& g, int dtype, const void* qbuf, cons
     *merge = true;
     return launch_decode_attn(g, qbuf, a, part, lc, l0, s);
   }
-  if (!attn_mfma_ok(g, dtype)) return hipSuccess;
+  if (!attn_mfma_ok(g, dtype, a)) return hipSuccess;
   *done = true;
   return launch_attn_prefill(g, qbuf, a, o, l0, lc, s);
 }
