@@ -21,16 +21,15 @@
 // than 8 (a factor 2^8), so the accumulator rescale is rare.
 //
 // Staging: K and V tiles stream straight from the pool into LDS
-// (global_load_lds_dwordx4) through 4 stages, unpadded 256-byte key rows with
-// the 16-byte chunk c of row r stored at slot c ^ (r & 15), so that 16
-// consecutive rows read at one chunk hit distinct bank groups.  V stays key
-// major; its operand (4 consecutive keys of one channel per half) is read
+// (global_load_lds_dwordx4) through 4 stages as unpadded 256-byte key rows
+// whose 16-byte chunks are permuted per row (kswz, vswz) so that the reads
+// below hit every bank group evenly.  V stays key major; its operand (4 consecutive keys of one channel per half) is read
 // with ds_read_b64_tr_b16: within each group of 16 lanes, lane i addressing
 // row key0 + i / 4, channels c0 + 4 (i % 4) .. + 3 receives keys
 // key0 .. key0 + 3 of channel c0 + i.
 //
 // Software pipeline: iteration t issues the QK^T products of tile t + 1
-// before the softmax of tile t, so that the matrix cores work on the next
+// before the softmax of tile t, so that the matrix cores can work on the next
 // scores while the vector ALUs exponentiate the current ones; then the PV
 // products of tile t.
 //
@@ -61,6 +60,15 @@ constexpr int kPTile = kKT * kDh;   // elements of one K (or V) tile
 constexpr int kXcd = 8;             // XCDs per device
 constexpr size_t kLdsMax = 160 * 1024;
 constexpr size_t kStaticLds = (size_t)kPS * 2 * kPTile * 2;
+
+// LDS slot permutations of a key row's 16 chunks of 16 bytes.  K rows are
+// read 16 consecutive rows at one chunk: chunk c of row r sits at slot
+// c ^ (r & 15).  V rows are read transposed, 8 consecutive rows x 4 adjacent
+// chunks per instruction: chunk c of row r sits at slot c ^ vswz(r), with
+// vswz the 2-bit rotation of r & 15, which sends those 32 (row, chunk) pairs
+// to every slot exactly twice.
+__device__ inline int kswz(int r) { return r & 15; }
+__device__ inline int vswz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 
 __device__ inline uint32_t cvt2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2){a, b}, bf16x2));
@@ -141,9 +149,10 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const int id = __builtin_amdgcn_readfirstlane(s_tbl[key0 >> g.b_shift]);
         const char* kb = (const char*)pool +
                          ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
-        const uint32_t vo =
-            (lane >> 4) * (kDh * 2) + (((lane & 15) ^ ((j * 4 + (lane >> 4)) & 15)) * 16);
-        lds_dma16_sv(kb, vo, kl + j * 1024);
+        const int r = j * 4 + (lane >> 4);
+        const uint32_t ko = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ kswz(r)) * 16);
+        const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ vswz(r)) * 16);
+        lds_dma16_sv(kb, ko, kl + j * 1024);
         lds_dma16_sv(kb + kv_gap, vo, vl + j * 1024);
       }
     } else {
@@ -153,12 +162,11 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int jj = 0; jj < 2; ++jj) {
         const int j = wave + jj * kPW;
         const int r = j * 4 + (lane >> 4);
-        const int c = (lane & 15) ^ (r & 15);
         const int key = min(tile * kKT + r, key_end - 1);
         const int64_t base = (int64_t)s_tbl[key >> g.b_shift] * g.block_elems +
-                             (key & (g.B - 1)) * kDh + c * 8;
-        lds_dma16(pool + base + koff, Ks + j * 512);
-        lds_dma16(pool + base + voff, Vs + j * 512);
+                             (key & (g.B - 1)) * kDh;
+        lds_dma16(pool + base + koff + ((lane & 15) ^ kswz(r)) * 8, Ks + j * 512);
+        lds_dma16(pool + base + voff + ((lane & 15) ^ vswz(r)) * 8, Vs + j * 512);
       }
     }
   };
@@ -172,7 +180,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       const int r = kt * 32 + col;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ (r & 15)) * 8));
+        const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ kswz(r)) * 8));
         sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
       }
     }
@@ -186,28 +194,30 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   float m_run = -INFINITY, l_run = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // Copies of one wave complete in order, 4 per tile: tile t is ready once at
+  // Copies of one wave complete in order, 4 per tile: a tile is ready once at
   // most the 4 k copies of the k tiles issued after it are pending.
+  static_assert(kPS >= 3 && kPS <= 4, "stages");
+  auto wait_tiles = [](int k) {
+    if (k >= 2)
+      wait_vmcnt<8>();
+    else if (k == 1)
+      wait_vmcnt<4>();
+    else
+      wait_vmcnt<0>();
+  };
   for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
-  if (n_tiles > 2)
-    wait_vmcnt<8>();
-  else if (n_tiles == 2)
-    wait_vmcnt<4>();
-  else
-    wait_vmcnt<0>();
+  wait_tiles(min(kPS - 1, n_tiles) - 1);
   lds_barrier();
   floatx16 sacc[2];
   qk(0, sacc);
 
   for (int tile = 0; tile < n_tiles; ++tile) {
+    const bool has_next = tile + 1 < n_tiles;
     floatx16 snext[2];
-    if (tile + 1 < n_tiles) {
+    if (has_next) {
       // tile + 1 ready, and every wave is done with tile - 1, whose buffer
       // is refilled
-      if (tile + 2 < n_tiles)
-        wait_vmcnt<4>();
-      else
-        wait_vmcnt<0>();
+      wait_tiles(min(tile + kPS - 1, n_tiles) - (tile + 2));
       lds_barrier();
       if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
       qk((tile + 1) % kPS, snext);
@@ -276,16 +286,16 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const int dc = mt * 32 + (gi & 1) * 16 + (li & 3) * 4;
         const int ch = dc >> 3, hf = (dc & 7);
         const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_a * kDh + ((ch ^ (key_a & 15)) * 8) + hf));
+            KV_LDS4(Vs + key_a * kDh + ((ch ^ vswz(key_a)) * 8) + hf));
         const int key_b = key_a + 8;
         const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_b * kDh + ((ch ^ (key_b & 15)) * 8) + hf));
+            KV_LDS4(Vs + key_b * kDh + ((ch ^ vswz(key_b)) * 8) + hf));
         const v4s vv[2] = {r0, r1};
         oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf[s4],
                                                            oacc[mt], 0, 0, 0);
       }
     }
-    if (tile + 1 < n_tiles) {
+    if (has_next) {
       sacc[0] = snext[0];
       sacc[1] = snext[1];
     }

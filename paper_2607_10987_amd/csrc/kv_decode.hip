@@ -44,6 +44,12 @@ struct DecodeUnit {
   uint32_t mask_lo, mask_hi;
 };
 
+// LDS slot of chunk c of key row r: c ^ kswz(r) for K (read 16 rows at one
+// chunk), c ^ vswz(r) for V (read transposed, 8 rows x 4 adjacent chunks);
+// both spread each read over all bank groups.
+__device__ inline int kswz(int r) { return r & 15; }
+__device__ inline int vswz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
 __device__ inline uint32_t pack2(float a, float b) {
   const __bf16 x = (__bf16)a, y = (__bf16)b;
   return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
@@ -212,8 +218,9 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const char* kb = (const char*)pool +
                          ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
         const int r = j * 4 + (lane >> 4);
-        const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ (r & 15)) * 16);
-        lds_dma16_sv(kb, vo, ks_lds + j * 1024);
+        const uint32_t ko = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ kswz(r)) * 16);
+        const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ vswz(r)) * 16);
+        lds_dma16_sv(kb, ko, ks_lds + j * 1024);
         lds_dma16_sv(kb + kv_gap, vo, ks_lds + kKT * kDh * 2 + j * 1024);
       }
     };
@@ -261,7 +268,7 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         for (int e = 0; e < 16; ++e) sacc[rt][e] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(Ks + col * kDh + (((ks * 2 + hl) ^ (col & 15)) * 8));
+        const bf16x8 kf = *(const bf16x8*)(Ks + col * kDh + (((ks * 2 + hl) ^ kswz(col)) * 8));
         sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], sacc[0], 0, 0, 0);
         if (two)
           sacc[RT - 1] =
@@ -321,9 +328,9 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
           const int dc = mt * 32 + (g4 & 1) * 16 + (li & 3) * 4;
           const int ch = dc >> 3, hf = dc & 7;
           const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              KV_LDS4(Vs + key_a * kDh + ((ch ^ (key_a & 15)) * 8) + hf));
+              KV_LDS4(Vs + key_a * kDh + ((ch ^ vswz(key_a)) * 8) + hf));
           const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              KV_LDS4(Vs + key_b * kDh + ((ch ^ (key_b & 15)) * 8) + hf));
+              KV_LDS4(Vs + key_b * kDh + ((ch ^ vswz(key_b)) * 8) + hf));
           const v4s vv[2] = {r0, r1};
           const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
           oacc[0][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[0][s4], oacc[0][mt], 0, 0, 0);
