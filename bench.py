@@ -26,6 +26,7 @@ Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu]
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -70,6 +71,30 @@ def kv_bytes_per_token(s):
 
 
 # ------------------------------------------------------------------ cpu baseline
+
+def measured_traffic(workload, kind):
+    """HBM bytes per launch of a kernel kind, from the committed rocprofv3 PMC
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a plain copy's reading), or
+    None when there is none or the kernel's source changed since."""
+    path = os.path.join(ROOT, "profiles", f"pmc_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    try:
+        entry = json.loads(text[start + 7:end])["kinds"].get(kind)
+    except (ValueError, KeyError):
+        return None
+    if not entry:
+        return None
+    with open(os.path.join(ROOT, entry["source"]), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != entry["source_sha256"]:
+            return None
+    return entry["hbm_bytes_per_dispatch"]
+
 
 def cpu_baseline(wl, seed):
     """The float64 oracle on a bounded sample: one layer of the workload's shape,
@@ -273,7 +298,10 @@ def main():
     else:
         achieved, peak, unit = work * K / t_dom / 1e9, HBM_PEAK_GBS, "GB/s"
     roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "unit": unit, "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic(wl.name, dom),
+                "algorithmic_bytes_per_launch": int(work / max(prof[dom][0] // K, 1))
+                if bound == "hbm" else None,
                 "launches_per_step": prof[dom][0] // K,
                 "avg_launch_ms": round(prof[dom][1] / max(prof[dom][0], 1), 4)}
 

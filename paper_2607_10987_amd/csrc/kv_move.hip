@@ -127,20 +127,143 @@ struct Vec<float> {  // 4 per 16 bytes
   __device__ static void set(uint4& v, int i, float f) { (&v.x)[i] = __float_as_uint(f); }
 };
 
-// grid (n_dest_blocks, L).  Destination block b of the new state takes token
+// Destination blocks that compose copies (those not aliased to a source
+// block), as runs [b0[k], b0[k] + (cum[k + 1] - cum[k])) of consecutive ids.
+struct CopyRuns {
+  int32_t n;
+  int32_t b0[KV_MAX_SEGMENTS + 1];
+  int32_t cum[KV_MAX_SEGMENTS + 2];
+};
+
+// Per-row source of destination block b (rows r < B): source block id, slot
+// and key shift; src = -1 past the end of the composed state.
+__device__ inline void compose_rows(const PoolGeom& g, const ComposeArgs& a, int b, int32_t* s_src,
+                                    int32_t* s_slot, int32_t* s_delta) {
+  for (int r = threadIdx.x; r < g.B; r += kMoveThreads) {
+    const int u = b * g.B + r;
+    int32_t src = -1, slot = 0, delta = 0;
+    if (u < a.n_tokens) {
+      int i = 0;
+      while (i + 1 < a.nseg && a.seg[i + 1].cum <= u) ++i;
+      const int j = u - a.seg[i].off;
+      src = g.tables[(int64_t)a.seg[i].slot * g.max_blocks + j / g.B];
+      slot = j % g.B;
+      delta = a.seg[i].delta;
+    }
+    s_src[r] = src;
+    s_slot[r] = slot;
+    s_delta[r] = delta;
+  }
+}
+
+__device__ inline int copy_run_block(const CopyRuns& cr, int i) {
+  int k = 0;
+  while (k + 1 < cr.n && cr.cum[k + 1] <= i) ++k;
+  return cr.b0[k] + (i - cr.cum[k]);
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline void st_nt16(uint16_t* p, const uint4& v) {
+  __builtin_nontemporal_store((u32x4_t){v.x, v.y, v.z, v.w}, (u32x4_t*)p);
+}
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+
+__device__ inline uint32_t cvt_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t){a, b}, bf16x2_t));
+}
+
+// bf16 compose copy.  grid (copied blocks, L), one workgroup per (block,
+// layer) slab.  Work items are 16-byte chunks of key / value rows, a row's
+// chunks on consecutive lanes (1 KiB per wavefront access).  Destination
+// token u = b * B + r comes from segment i (source token u - off_i); keys of
+// a shifted segment are rotated by its shift delta: for frequency index j the
+// pair (x_j, x_{j + dh/2}) becomes (x cos - y sin, x sin + y cos) with
+// cos / sin of |delta| * theta_j (sin negated for a negative shift).  The two
+// halves of a row sit cpr / 2 lanes apart and are exchanged with a lane
+// shuffle.  All loads of a thread are issued before its stores.
+__global__ void __launch_bounds__(kMoveThreads)
+k_compose_bf16(PoolGeom g, ComposeArgs a, CopyRuns runs) {
+  constexpr int U = 8;  // items per thread per operand and pass
+  __shared__ int32_t s_src[64], s_slot[64], s_delta[64];
+  const int b = copy_run_block(runs, blockIdx.x), l = blockIdx.y;
+  const int tid = threadIdx.x;
+  compose_rows(g, a, b, s_src, s_slot, s_delta);
+  const int32_t dst = g.tables[(int64_t)a.new_slot * g.max_blocks + b];
+  __syncthreads();
+  uint16_t* pool = (uint16_t*)g.pool;
+  uint16_t* dblk = pool + (int64_t)dst * g.block_elems;
+  const int cpr = g.dh / 8, hc = cpr / 2, half = g.dh / 2;  // chunks per row, per half row
+  const int n_items = g.Hkv * g.B * cpr;                    // per operand
+  for (int base = 0; base < n_items; base += kMoveThreads * U) {
+    uint4 kx[U], vx[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = base + u * kMoveThreads + tid;
+      const int c = it % cpr, r = (it / cpr) % g.B, h = it / (cpr * g.B);
+      const int32_t src = it < n_items ? s_src[r] : -1;
+      kx[u] = vx[u] = make_uint4(0, 0, 0, 0);
+      if (src >= 0) {
+        const uint16_t* sb = pool + (int64_t)src * g.block_elems + c * 8;
+        kx[u] = *(const uint4*)(sb + tile_off(g, l, 0, h, s_slot[r]));
+        vx[u] = *(const uint4*)(sb + tile_off(g, l, 1, h, s_slot[r]));
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = base + u * kMoveThreads + tid;
+      const int c = it % cpr, r = (it / cpr) % g.B, h = it / (cpr * g.B);
+      // partner half of the row (all lanes take part in the shuffle)
+      uint4 px;
+      px.x = __shfl_xor(kx[u].x, hc);
+      px.y = __shfl_xor(kx[u].y, hc);
+      px.z = __shfl_xor(kx[u].z, hc);
+      px.w = __shfl_xor(kx[u].w, hc);
+      if (it >= n_items || s_src[r] < 0) continue;
+      const int delta = s_delta[r];
+      uint4 ko = kx[u];
+      if (delta != 0) {
+        const int ad = delta < 0 ? -delta : delta;
+        const bool lo = c < hc;
+        const float sg = (delta < 0) == lo ? 1.f : -1.f;  // sign of sin on the partner
+        const float* cp = g.rope_cos + (int64_t)ad * half + (c % hc) * 8;
+        const float* sp = g.rope_sin + (int64_t)ad * half + (c % hc) * 8;
+        const float4 c0 = *(const float4*)cp, c1 = *(const float4*)(cp + 4);
+        const float4 s0 = *(const float4*)sp, s1 = *(const float4*)(sp + 4);
+        const float cs[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        const uint32_t ow[4] = {kx[u].x, kx[u].y, kx[u].z, kx[u].w};
+        const uint32_t pw[4] = {px.x, px.y, px.z, px.w};
+        uint32_t rw[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float o0 = __uint_as_float(ow[q] << 16), o1 = __uint_as_float(ow[q] & 0xffff0000u);
+          const float p0 = __uint_as_float(pw[q] << 16), p1 = __uint_as_float(pw[q] & 0xffff0000u);
+          rw[q] = cvt_bf16x2(fmaf(p0, sg * sn[2 * q], o0 * cs[2 * q]),
+                             fmaf(p1, sg * sn[2 * q + 1], o1 * cs[2 * q + 1]));
+        }
+        ko = make_uint4(rw[0], rw[1], rw[2], rw[3]);
+      }
+      uint16_t* db = dblk + c * 8;
+      st_nt16(db + tile_off(g, l, 0, h, r), ko);
+      st_nt16(db + tile_off(g, l, 1, h, r), vx[u]);
+    }
+  }
+}
+
+// fp32 pools.  grid (copied blocks, L).  Destination block b of the new state takes token
 // u = b*B + r from segment i (source token u - off_i).  Keys are rotated by
 // the segment's shift delta: pair (x_i, x_{i+dh/2}) -> (x cos - y sin,
 // x sin + y cos) with cos/sin of |delta| * theta_i from the float table
 // (sin negated for a negative shift).  Values and unshifted keys are copied.
 template <typename T>
 __global__ void __launch_bounds__(kMoveThreads)
-k_compose_copy(PoolGeom g, ComposeArgs a) {
+k_compose_copy(PoolGeom g, ComposeArgs a, CopyRuns runs) {
   constexpr int V = Vec<T>::N;
   __shared__ int32_t s_src[64], s_slot[64], s_delta[64];
   __shared__ int32_t s_dst;
-  const int b = blockIdx.x, l = blockIdx.y;
-  for (int i = 0; i < a.nseg; ++i)
-    if (b >= a.seg[i].alias_b0 && b < a.seg[i].alias_b1) return;  // aliased, nothing to copy
+  const int b = copy_run_block(runs, blockIdx.x), l = blockIdx.y;
   if (threadIdx.x < g.B) {
     const int r = threadIdx.x;
     const int u = b * g.B + r;
@@ -236,12 +359,32 @@ hipError_t launch_cow(const PoolGeom& g, int dtype, const int2* cow_pairs, const
 
 hipError_t launch_compose_copy(const PoolGeom& g, int dtype, const ComposeArgs& a,
                                hipStream_t s) {
-  if (a.n_dest_blocks <= 0) return hipSuccess;
-  dim3 grid(a.n_dest_blocks, g.L);
-  if (dtype == KV_DTYPE_BF16)
-    k_compose_copy<uint16_t><<<grid, kMoveThreads, 0, s>>>(g, a);
+  // copied blocks: [0, n_dest_blocks) minus the (increasing, disjoint) alias ranges
+  CopyRuns runs;
+  runs.n = 0;
+  int32_t next = 0, total = 0;
+  auto add = [&](int32_t b0, int32_t b1) {
+    if (b1 <= b0) return;
+    runs.b0[runs.n] = b0;
+    runs.cum[runs.n] = total;
+    total += b1 - b0;
+    ++runs.n;
+  };
+  for (int i = 0; i < a.nseg; ++i) {
+    if (a.seg[i].alias_b1 <= a.seg[i].alias_b0) continue;
+    add(next, a.seg[i].alias_b0);
+    next = a.seg[i].alias_b1;
+  }
+  add(next, a.n_dest_blocks);
+  runs.cum[runs.n] = total;
+  if (total == 0) return hipSuccess;
+  dim3 grid(total, g.L);
+  if (dtype == KV_DTYPE_BF16 && g.dh >= 16 && (g.dh & (g.dh - 1)) == 0)
+    k_compose_bf16<<<grid, kMoveThreads, 0, s>>>(g, a, runs);
+  else if (dtype == KV_DTYPE_BF16)
+    k_compose_copy<uint16_t><<<grid, kMoveThreads, 0, s>>>(g, a, runs);
   else
-    k_compose_copy<float><<<grid, kMoveThreads, 0, s>>>(g, a);
+    k_compose_copy<float><<<grid, kMoveThreads, 0, s>>>(g, a, runs);
   return hipGetLastError();
 }
 
