@@ -208,7 +208,8 @@ def main():
     def step():
         root = kv.kv_materialize(pool.h, x_ctx, ctx, 0, o_ctx)
         kids = kv.kv_fork(pool.h, root, A)
-        kv.kv_attend(pool.h, kids, x_suf, suf, o_suf)
+        if suf:
+            kv.kv_attend(pool.h, kids, x_suf, suf, o_suf)
         for i in range(ndec):
             kv.kv_attend(pool.h, kids, x_dec[i], 1, o_dec)
         segs = [(root, 0, ctx)] + [(k, ctx, ctx + cont) for k in kids]

@@ -421,7 +421,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // element is used by one wavefront only, so operands are loaded straight from
 // global memory in the v_mfma_f32_16x16x32_bf16 layout (a lane reads 16 bytes
 // of one weight row; the four lanes of a row cover 64 contiguous bytes),
-// sixteen k-steps of loads in flight per lane.  Workgroup = one 128-channel
+// sixteen k-steps of loads in flight per lane (non-temporal loads measured
+// slower here).  Workgroup = one 128-channel
 // head of one layer, eight waves of 16 channels (so that the launch, 1536
 // workgroups for the 8B shape, fills the GPU in whole rounds); RoPE and the
 // stores go through an fp32 tile in LDS.  grid (N / 128, 1, lc), block 512.

