@@ -6,8 +6,8 @@
 // All of them are HBM-bound streams.  One workgroup moves one (block, layer)
 // slab of 2 * Hkv * B * dh elements (64 KiB for an 8B-shaped bf16 block with
 // B = 16), using 16-byte vector accesses and several independent loads in
-// flight per thread.  Loads and stores are non-temporal: every byte is moved
-// once, and streaming it past the caches measured 10-15% faster on MI355X.
+// flight per thread.  Every byte is moved once; streaming loads (and most
+// stores) past the caches with non-temporal accesses measured 5-15% faster.
 #include "kv_internal.h"
 
 namespace kvs {
@@ -53,7 +53,9 @@ __device__ inline PieceIdx piece_idx(int pieces, int L) {
 
 // Copy piece `piece` of a slab of n16 16-byte chunks; chunk c belongs to
 // slot (c / row16) % B and is replaced by zeros when that slot is >= valid.
-// Both sides are streamed with non-temporal accesses.
+// Loads are non-temporal; stores too unless PLAIN_ST (measured faster for the
+// scattered pool-block writes of unpack).
+template <bool PLAIN_ST = false>
 __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                   int piece, int n16, int row16, int B, int valid) {
   const int c0 = piece * (kPiece / 16) + threadIdx.x;
@@ -69,7 +71,7 @@ __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restri
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     const int c = c0 + u * kMoveThreads;
-    if (c < n16) st_nt(dst + c, v[u]);
+    if (c < n16) { if (PLAIN_ST) dst[c] = v[u]; else st_nt(dst + c, v[u]); }
   }
 }
 
@@ -101,8 +103,8 @@ k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src) 
   const int32_t id = trow[i];
   const char* s = src + i * block_bytes + l * layer_bytes;
   char* d = (char*)g.pool + id * block_bytes + l * layer_bytes;
-  copy_piece((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16), g.dh * elt / 16, g.B,
-             g.B);
+  copy_piece<true>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
+                   g.dh * elt / 16, g.B, g.B);
 }
 
 // grid (n_req, L): for requests with cow > 0, copy slots [0, cow) of every
