@@ -504,6 +504,91 @@ k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restr
   }
 }
 
+// Decode-size projection with the token rows staged in LDS (M <= 16 rows
+// whose padded copy fits): the x operand is read from LDS (row stride d + 8
+// elements, so the 16 rows one operand read touches fall in distinct bank
+// groups) instead of being fetched again from L2 by every wavefront, and the
+// next batch of weight loads is issued before the products of the current
+// one.  Same tiling as k_qkv_decode<1>; dynamic LDS: M * (d + 8) bf16.
+constexpr int kDecU = 8;  // k-steps of 32 per load batch (two batches in flight)
+
+__global__ void __launch_bounds__(64 * kDecWaves)
+k_qkv_decode_lds(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
+                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
+  constexpr int FLD = kDh + 4;
+  constexpr int NT = 64 * kDecWaves;
+  __shared__ __attribute__((aligned(16))) float Cf[16 * FLD];
+  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][d + 8]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  const int n0 = blockIdx.x * kDh;
+  const int lc = blockIdx.z, l = l0 + lc;
+  const int M = a.batch * a.T, d = g.d, xld = d + 8;
+  const uint16_t* wl = w + (int64_t)l * w_stride;
+  const uint16_t* wr = wl + (int64_t)(n0 + wave * 16 + lr) * d + lk;
+
+  // weights of the first batch, then the token rows into LDS
+  uint4 fa[kDecU], fn[kDecU];
+#pragma unroll
+  for (int u = 0; u < kDecU; ++u) fa[u] = *(const uint4*)(wr + 32 * u);
+  const int d8 = d / 8;
+  for (int i = tid; i < M * d8; i += NT) {
+    const int r = i / d8, c = i - r * d8;
+    *(uint4*)(xs + r * xld + c * 8) = *(const uint4*)(x + (int64_t)r * d + c * 8);
+  }
+  __syncthreads();
+  const bool xok = lr < M;
+  const uint16_t* xr = xs + (xok ? lr : 0) * xld + lk;
+
+  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < d; k0 += 32 * kDecU) {
+    const bool more = k0 + 32 * kDecU < d;
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < kDecU; ++u) fn[u] = *(const uint4*)(wr + k0 + 32 * kDecU + 32 * u);
+    }
+#pragma unroll
+    for (int u = 0; u < kDecU; ++u) {
+      const uint4 fb = xok ? *(const uint4*)(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa[u]),
+                                                    __builtin_bit_cast(bf16x8v, fb), acc, 0, 0, 0);
+    }
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < kDecU; ++u) fa[u] = fn[u];
+    }
+  }
+  // C[16 ch x 16 tok]: lane holds channels 4 (lane / 16) + e of token lane % 16
+  {
+    const int ch = wave * 16 + (lane >> 4) * 4;
+    *(float4*)(Cf + lr * FLD + ch) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+  __syncthreads();
+  const int half = kDh / 2;
+  const int hh = n0 / kDh;
+  for (int it = tid; it < 16 * (half / 4); it += NT) {
+    const int f4 = it % (half / 4), r = it / (half / 4);
+    if (r >= M) continue;
+    const float4 xv = *(const float4*)(Cf + r * FLD + f4 * 4);
+    const float4 yv = *(const float4*)(Cf + r * FLD + half + f4 * 4);
+    float4 xo = xv, yo = yv;
+    if (hh < g.Hq + g.Hkv) {
+      const int pos = row_info(a, r).pos;
+      const float4 cs = *(const float4*)(g.rope_cos + (int64_t)pos * half + f4 * 4);
+      const float4 sn = *(const float4*)(g.rope_sin + (int64_t)pos * half + f4 * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float c = (&cs.x)[q], s = (&sn.x)[q];
+        (&xo.x)[q] = (&xv.x)[q] * c - (&yv.x)[q] * s;
+        (&yo.x)[q] = (&xv.x)[q] * s + (&yv.x)[q] * c;
+      }
+    }
+    uint16_t* dp = dest(g, a, qbuf, lc, l, M, r, hh, f4 * 4);
+    *(uint2*)dp = make_uint2(pack_bf16x2(xo.x, xo.y), pack_bf16x2(xo.z, xo.w));
+    *(uint2*)(dp + half) = make_uint2(pack_bf16x2(yo.x, yo.y), pack_bf16x2(yo.z, yo.w));
+  }
+}
+
 }  // namespace
 
 bool qkv_mfma_ok(const PoolGeom& g, int dtype) {
@@ -515,7 +600,12 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
                            const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s) {
   const int M = a.batch * a.T;
   const int N = (g.Hq + 2 * g.Hkv) * kDh;
-  if (M <= 16 && g.d % 512 == 0) {
+  const size_t x_lds = (size_t)M * (g.d + 8) * 2;
+  if (M <= 16 && g.d % (32 * kDecU) == 0 && x_lds + 16 * (kDh + 4) * 4 <= 160 * 1024) {
+    dim3 grid(N / kDh, 1, lc);
+    k_qkv_decode_lds<<<grid, 64 * kDecWaves, x_lds, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
+                                                         w_stride, a, (uint16_t*)qbuf, l0);
+  } else if (M <= 16 && g.d % 512 == 0) {
     dim3 grid(N / kDh, 1, lc);
     k_qkv_decode<1><<<grid, 64 * kDecWaves, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
                                                    w_stride, a, (uint16_t*)qbuf, l0);
