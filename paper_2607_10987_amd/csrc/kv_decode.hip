@@ -206,7 +206,8 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int ks = 0; ks < 8; ++ks) settle(qf[rt][ks]);
 
     // stage loads: 8 copies of 1 KiB (4 key rows, all in one block since
-    // B >= 16) per operand, block base in scalar registers.  Rows past the
+    // B >= 16) per operand, block base in scalar registers, non-temporal
+    // (each byte is read once per call).  Rows past the
     // unit's last key read slots of a real block; their scores are masked and
     // their V rows zeroed in LDS before use.
     auto issue = [&](int tile, int buf) {
@@ -220,8 +221,8 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const int r = j * 4 + (lane >> 4);
         const uint32_t ko = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ kswz(r)) * 16);
         const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ vswz(r)) * 16);
-        lds_dma16_sv(kb, ko, ks_lds + j * 1024);
-        lds_dma16_sv(kb + kv_gap, vo, ks_lds + kKT * kDh * 2 + j * 1024);
+        lds_dma16_sv_nt(kb, ko, ks_lds + j * 1024);
+        lds_dma16_sv_nt(kb + kv_gap, vo, ks_lds + kKT * kDh * 2 + j * 1024);
       }
     };
 

@@ -47,6 +47,14 @@ __device__ inline void lds_dma16_sv(const void* sbase, uint32_t voff, uint32_t l
                : "memory", "m0");
 }
 
+// lds_dma16_sv with the non-temporal cache policy (data read exactly once).
+__device__ inline void lds_dma16_sv_nt(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
 template <int N>
 __device__ inline void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
