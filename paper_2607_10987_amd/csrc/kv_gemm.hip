@@ -342,26 +342,32 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
     if (kb + kDlStages - 1 < nk) issue(kb + kDlStages - 1, (kb + kDlStages - 1) % kDlStages);
     const uint16_t* As = smem + (kb % kDlStages) * STAGE;
     const uint16_t* Bs = As + OP;
+    // all operands of the stage first, so that only the first products wait
+    // for LDS
+    constexpr int KS = kDlBK / 16;
+    bf16x8 fa[KS][TI], fb[KS][TJ];
 #pragma unroll
-    for (int ks = 0; ks < kDlBK / 16; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       const int q = ks * 2 + hl;
-      bf16x8 fa[TI], fb[TJ];
 #pragma unroll
       for (int i = 0; i < TI; ++i) {
         const int m = ch0 + i * 32 + (lane & 31);
-        fa[i] = *(const bf16x8*)(As + (m * 4 + (q ^ swz(m))) * 8);
+        fa[ks][i] = *(const bf16x8*)(As + (m * 4 + (q ^ swz(m))) * 8);
       }
 #pragma unroll
       for (int j = 0; j < TJ; ++j) {
         const int t = tk0 + j * 32 + (lane & 31);
-        fb[j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ swz(t))) * 8);
+        fb[ks][j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ swz(t))) * 8);
       }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
   }
   __syncthreads();  // LDS stages become the epilogue's staging tile
 
