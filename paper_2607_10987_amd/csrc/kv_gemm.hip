@@ -263,19 +263,18 @@ k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restric
 
 // Prefill projection, main loop with direct global->LDS loads
 // (global_load_lds_dwordx4: lane i of a wavefront writes LDS bytes
-// [16 i, 16 i + 16) of the instruction's 1 KiB destination) and a 4-stage
-// pipeline: three K-steps of 32 are in flight while the fourth is consumed,
-// with no register staging.  Tile 256 channels x 256 tokens, 8 wavefronts of
-// 128 channels x 64 tokens (a wave owns a whole head, so RoPE stays in
-// registers).  LDS rows are 64 bytes (32 k); the 16-byte chunk q of row r is
-// stored at chunk slot q ^ f(r), f(r) = (r >> 2) & 3: the 16 consecutive
-// rows one LDS cycle serves of an operand read (16 lanes x 16 bytes over 64
-// banks) then cover all 16 bank groups; measured free of bank conflicts,
-// unlike ((r >> 1) ^ (r >> 3)) & 3.
-__device__ inline int swz(int r) { return (r >> 2) & 3; }
+// [16 i, 16 i + 16) of the instruction's 1 KiB destination) and a 2-stage
+// pipeline of K-steps of 64: one step is in flight while the other is
+// consumed, with no register staging.  Tile 256 channels x 256 tokens, 8
+// wavefronts of 128 channels x 64 tokens (a wave owns a whole head, so RoPE
+// stays in registers).  LDS rows are 128 bytes (64 k); the 16-byte chunk q of
+// row r is stored at chunk slot q ^ f(r), f(r) = (r >> 1) & 7, so that the 16
+// consecutive rows an operand read serves in one LDS cycle (16 lanes x 16
+// bytes over 64 banks) cover the 16 bank groups.
+__device__ inline int swz(int r) { return (r >> 1) & 7; }
 
-constexpr int kDlStages = 4;
-constexpr int kDlBK = 32;
+constexpr int kDlStages = 2;
+constexpr int kDlBK = 64;
 constexpr int kDlWaves = 8;
 constexpr int kDlThreads = 64 * kDlWaves;
 
@@ -306,7 +305,7 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
   const uint16_t* gb[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
-    const int c = (wave * LPW + j) * 64 + lane, r = c >> 2, q = (c & 3) ^ swz(r);
+    const int c = (wave * LPW + j) * 64 + lane, r = c >> 3, q = (c & 7) ^ swz(r);
     ga[j] = wl + (int64_t)(n0 + r) * d + q * 8;
     gb[j] = x + (int64_t)min(m0 + r, M - 1) * d + q * 8;  // rows past M: any valid row
   }
@@ -335,7 +334,7 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
     // stages (2 x 2 LPW instructions) are outstanding; the barrier extends
     // that to every wave's share of the stage
     if (kb + kDlStages - 2 < nk)
-      wait_vmcnt<2 * 2 * LPW>();
+      wait_vmcnt<(kDlStages - 2) * 2 * LPW>();
     else
       wait_vmcnt<0>();
     lds_barrier();
@@ -352,12 +351,12 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
 #pragma unroll
       for (int i = 0; i < TI; ++i) {
         const int m = ch0 + i * 32 + (lane & 31);
-        fa[ks][i] = *(const bf16x8*)(As + (m * 4 + (q ^ swz(m))) * 8);
+        fa[ks][i] = *(const bf16x8*)(As + (m * 8 + (q ^ swz(m))) * 8);
       }
 #pragma unroll
       for (int j = 0; j < TJ; ++j) {
         const int t = tk0 + j * 32 + (lane & 31);
-        fb[ks][j] = *(const bf16x8*)(Bs + (t * 4 + (q ^ swz(t))) * 8);
+        fb[ks][j] = *(const bf16x8*)(Bs + (t * 8 + (q ^ swz(t))) * 8);
       }
     }
     __builtin_amdgcn_sched_barrier(0);
