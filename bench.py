@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device copy first (reference for HBM byte counters)")
+    ap.add_argument("--transfer-sweep", action="store_true",
+                    help="instead of the step: measured materialize vs pack + unpack per context "
+                         "length, and the transfer-vs-recompute decision at several link rates")
     return ap.parse_args()
 
 
@@ -143,6 +146,77 @@ class _Shape1:
         self.n_layers = 1
 
 
+
+# ------------------------------------------------------------------ transfer sweep
+
+LINKS = [("10 Gb/s", 1.25e9, 20e-6), ("25 Gb/s", 3.125e9, 20e-6), ("100 Gb/s", 12.5e9, 10e-6),
+         ("400 Gb/s", 50e9, 5e-6), ("xGMI link 153 GB/s", 153e9, 2e-6)]
+
+
+def transfer_sweep(args, kv, torch, synth):
+    """Single-GPU counterpart of the paper's transfer-vs-recomputation
+    experiment on the 8B shape: for each context length, materialize (the
+    recompute cost) and pack + unpack (the device side of a transfer) are
+    timed with the library's per-kernel events; the decision of
+    kv_plan_transfer is then reported for several link rates."""
+    wl = synth.WORKLOADS["fork4-8b"]
+    s = wl.shape
+    dev = "cuda"
+    tdt = torch.bfloat16
+    L, d, cols, B = s.n_layers, s.d_model, s.qkv_cols, s.block_size
+    lengths = [1024, 2048, 4096, 8192, 16384, 32768]
+    nmax = lengths[-1]
+    cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, nmax + 64, 8,
+                      s.rope_base, 1)
+    n_blocks = 2 * (nmax // B) + 64
+    pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, nmax, 1, nmax + 64))
+    w = torch.empty((L, cols, d), dtype=tdt, device=dev)
+    for layer in range(L):
+        w[layer] = synth.normal_torch(synth.w_key(args.seed, wl.name, layer), (cols, d), s.w_std,
+                                      s.dtype, dev)
+    pool.set_weights(w, cols * d)
+    x = synth.normal_torch(synth.x_key(args.seed, wl.name, 0), (nmax, d), 1.0, s.dtype, dev)
+    o = torch.empty((L, nmax, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
+    buf = torch.empty((nmax // B) * s.block_bytes, dtype=torch.uint8, device=dev)
+    rows = []
+    for n in lengths:
+        times = {"mat": [], "pack": [], "unpack": []}
+        for rep in range(3):
+            kv.kv_profile_enable(pool.h, True)
+            kv.kv_profile_read(pool.h)
+            st = kv.kv_materialize(pool.h, x[:n], n, 0, o[:, :n])
+            nb = kv.kv_state_info(pool.h, st)["n_blocks"]
+            hdr = kv.kv_pack(pool.h, st, 0, nb, buf)
+            u = kv.kv_unpack(pool.h, hdr, buf)
+            prof = kv.kv_profile_read(pool.h)
+            kv.kv_profile_enable(pool.h, False)
+            kv.kv_release(pool.h, st)
+            kv.kv_release(pool.h, u)
+            if rep == 0:
+                continue  # warm-up
+            times["mat"].append(sum(prof[k][1] for k in ("alloc", "qkv", "attn")))
+            times["pack"].append(prof["pack"][1])
+            times["unpack"].append(prof["unpack"][1])
+        t_mat = min(times["mat"]) / 1e3
+        t_pack = min(times["pack"]) / 1e3
+        t_unpack = min(times["unpack"]) / 1e3
+        kvb = (-(-n // B)) * s.block_bytes
+        fl = kv.kv_plan_transfer(cfg, n, 1.0, 0.0, 0.0, 0.0, 1.0)["prefill_flops"]
+        rate = fl / t_mat
+        row = {"tokens": n, "kv_bytes": kvb, "materialize_ms": round(t_mat * 1e3, 3),
+               "prefill_TFLOPs": round(rate / 1e12, 1), "pack_ms": round(t_pack * 1e3, 4),
+               "unpack_ms": round(t_unpack * 1e3, 4), "links": {}}
+        for name, bw, lat in LINKS:
+            plan = kv.kv_plan_transfer(cfg, n, bw, lat, kvb / t_pack, kvb / t_unpack, rate)
+            row["links"][name] = {"transfer_ms": round(plan["t_transfer"] * 1e3, 3),
+                                  "decision": "transfer" if plan["transfer"] else "recompute",
+                                  "speedup": round(plan["t_prefill"] / plan["t_transfer"], 2)}
+        rows.append(row)
+        print(f"[bench] sweep {n} tokens done", file=sys.stderr, flush=True)
+    pool.close()
+    print(json.dumps({"experiment": "transfer vs recompute (8B shape, one MI355X)",
+                      "data": "synthetic", "rows": rows}), flush=True)
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -157,6 +231,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU"}))
         sys.exit(2)
+    if args.transfer_sweep:
+        transfer_sweep(args, kv, torch, synth)
+        return
     wl = synth.WORKLOADS[args.workload]
     s = wl.shape
     ndec = wl.decode if args.decode is None else args.decode

@@ -238,6 +238,36 @@ typedef struct {
 kv_status kv_profile_enable(kv_pool* pool, int32_t enabled);
 kv_status kv_profile_read(kv_pool* pool, kv_profile_entry* out /* KV_KERNEL_KINDS */);
 
+/* Transfer-vs-recompute decision for a state of n_tokens tokens: the state-
+ * aware scheduling rule of the paper (pi(S) = transfer iff
+ * T_transfer < T_prefill, with T_transfer = |KV| / BW + delta, as in the
+ * first steps of the KV-Transfer algorithm).  Pure host arithmetic on
+ * caller-supplied rates (typically measured with kv_profile_*); touches no
+ * device memory and needs no pool.
+ *   kv_bytes      = ceil(n_tokens / B) * block bytes   (what kv_pack moves)
+ *   t_transfer    = kv_bytes / link_bytes_per_s + link_latency_s
+ *                   + kv_bytes / pack_bytes_per_s + kv_bytes / unpack_bytes_per_s
+ *                   (a pack or unpack rate <= 0 leaves that term out)
+ *   prefill_flops = L * (2 n d (Hq + 2 Hkv) dh + 4 Hq dh n (n + 1) / 2)
+ *                   (projections, and causal attention over visible pairs)
+ *   t_prefill     = prefill_flops / prefill_flops_per_s
+ *   transfer      = 1 iff t_transfer < t_prefill, else 0 (recompute).
+ * Errors: KV_ERR_ARG for a null pointer, an invalid cfg, n_tokens < 1,
+ * link_bytes_per_s <= 0, link_latency_s < 0 or prefill_flops_per_s <= 0. */
+typedef struct {
+  double kv_bytes;
+  double t_transfer; /* seconds */
+  double t_prefill;  /* seconds */
+  double prefill_flops;
+  int32_t transfer; /* 1 = transfer, 0 = recompute */
+  int32_t pad;
+} kv_transfer_plan;
+
+kv_status kv_plan_transfer(const kv_model_cfg* cfg, int64_t n_tokens, double link_bytes_per_s,
+                           double link_latency_s, double pack_bytes_per_s,
+                           double unpack_bytes_per_s, double prefill_flops_per_s,
+                           kv_transfer_plan* out);
+
 /* Human-readable name of a status. */
 const char* kv_strerror(kv_status status);
 

@@ -13,6 +13,7 @@ Modules
   pool       the paged block pool: FIFO free ring, refcounts, block tables,
              catalog, and the seven operators (materialize, fork, attend,
              compose, pack, unpack, evict) plus release and pin
+  policy     the transfer-vs-recompute decision of the scheduling rule
 
 Operator semantics follow the paper's stateful-operator section (state object
 S_KV = (M, Theta, B, Pi, Lambda, Gamma), Compat predicate, operator
@@ -26,3 +27,4 @@ from .attention import causal_gqa_attention, attention_rows  # noqa: F401
 from .model import project_qkv, project_kv, project_q, split_w  # noqa: F401
 from .pool import (OraclePool, OracleError, Status, Lineage,  # noqa: F401
                    PACK_MAGIC, PACK_VERSION)
+from .policy import kv_bytes, prefill_flops, plan_transfer  # noqa: F401

@@ -373,6 +373,35 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
 
 extern "C" {
 
+kv_status kv_plan_transfer(const kv_model_cfg* cfg, int64_t n_tokens, double link_bytes_per_s,
+                           double link_latency_s, double pack_bytes_per_s,
+                           double unpack_bytes_per_s, double prefill_flops_per_s,
+                           kv_transfer_plan* out) {
+  if (!out) return KV_ERR_ARG;
+  KV_TRY(check_cfg(cfg));
+  if (n_tokens < 1 || !(link_bytes_per_s > 0.0) || !(link_latency_s >= 0.0) ||
+      !(prefill_flops_per_s > 0.0))
+    return KV_ERR_ARG;
+  const kv_model_cfg& c = *cfg;
+  const double elt = c.dtype == KV_DTYPE_BF16 ? 2.0 : 4.0;
+  const double block_bytes =
+      2.0 * c.n_layers * c.n_kv_heads * (double)c.block_size * c.head_dim * elt;
+  const double n = (double)n_tokens;
+  kv_transfer_plan r;
+  std::memset(&r, 0, sizeof(r));
+  r.kv_bytes = (double)ceil_div(n_tokens, c.block_size) * block_bytes;
+  r.t_transfer = r.kv_bytes / link_bytes_per_s + link_latency_s;
+  if (pack_bytes_per_s > 0.0) r.t_transfer += r.kv_bytes / pack_bytes_per_s;
+  if (unpack_bytes_per_s > 0.0) r.t_transfer += r.kv_bytes / unpack_bytes_per_s;
+  const double cols = (double)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  r.prefill_flops = c.n_layers * (2.0 * n * c.d_model * cols +
+                                  4.0 * c.n_q_heads * c.head_dim * (n * (n + 1.0) / 2.0));
+  r.t_prefill = r.prefill_flops / prefill_flops_per_s;
+  r.transfer = r.t_transfer < r.t_prefill ? 1 : 0;
+  *out = r;
+  return KV_OK;
+}
+
 const char* kv_strerror(kv_status st) {
   switch (st) {
     case KV_OK: return "KV_OK";

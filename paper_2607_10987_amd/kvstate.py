@@ -94,6 +94,8 @@ _SIGS = {
     "kv_read_block_table": (_I32, [_P, _I64, _PI32, _I64, _P]),
     "kv_read_allocator": (_I32, [_P, _PI32, _PI32, _PI64, _PI64, _P]),
     "kv_strerror": (ctypes.c_char_p, [_I32]),
+    "kv_plan_transfer": (_I32, [_P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_double, _P]),
     "kv_profile_enable": (_I32, [_P, _I32]),
     "kv_profile_read": (_I32, [_P, ctypes.c_void_p]),
 }
@@ -293,6 +295,24 @@ def kv_read_allocator(pool, n_blocks: int, stream=None):
 
 KERNEL_KINDS = ["alloc", "fork", "release", "compose_meta", "compose_copy", "pack", "unpack",
                 "cow", "qkv", "qkv_decode", "attn", "attn_decode", "merge"]
+
+
+class kv_transfer_plan(ctypes.Structure):
+    _fields_ = [("kv_bytes", ctypes.c_double), ("t_transfer", ctypes.c_double),
+                ("t_prefill", ctypes.c_double), ("prefill_flops", ctypes.c_double),
+                ("transfer", ctypes.c_int32), ("pad", ctypes.c_int32)]
+
+
+def kv_plan_transfer(cfg: kv_model_cfg, n_tokens: int, link_bytes_per_s: float,
+                     link_latency_s: float, pack_bytes_per_s: float, unpack_bytes_per_s: float,
+                     prefill_flops_per_s: float) -> dict:
+    """Transfer-vs-recompute decision (host only; see include/kvstate.h)."""
+    out = kv_transfer_plan()
+    _check(lib().kv_plan_transfer(ctypes.byref(cfg), n_tokens, link_bytes_per_s, link_latency_s,
+                                  pack_bytes_per_s, unpack_bytes_per_s, prefill_flops_per_s,
+                                  ctypes.byref(out)), "kv_plan_transfer")
+    return {"kv_bytes": out.kv_bytes, "t_transfer": out.t_transfer, "t_prefill": out.t_prefill,
+            "prefill_flops": out.prefill_flops, "transfer": bool(out.transfer)}
 
 
 class kv_profile_entry(ctypes.Structure):
