@@ -273,12 +273,20 @@ def main():
     print(f"[bench] setup done in {time.perf_counter() - t_setup:.1f} s", file=sys.stderr,
           flush=True)
 
-    if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
+    # plain device copy of 1 GiB: reference rate for the HBM-bound operators
+    # (and, with --copy-calibration, the reference for HBM byte counters)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    copy_ms = []
+    for _ in range(1 if args.copy_calibration else 4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
         dst.copy_(src)
+        e1.record()
         torch.cuda.synchronize()
-        del src, dst
+        copy_ms.append(e0.elapsed_time(e1))
+    copy_gbs = 2.0 * (1 << 30) / (min(copy_ms[1:] or copy_ms) / 1e3) / 1e9
+    del src, dst
 
     info = {}
 
@@ -355,6 +363,9 @@ def main():
     put("compose", ["compose_copy"], b_compose, "GB/s", HBM_PEAK_GBS)
     put("pack", ["pack"], b_pack, "GB/s", HBM_PEAK_GBS)
     put("unpack", ["unpack"], b_unpack, "GB/s", HBM_PEAK_GBS)
+    for k in ("decode qkv", "decode attention", "compose", "pack", "unpack"):
+        if ops[k]["rate"] is not None:
+            ops[k]["frac_of_copy"] = round(ops[k]["rate"] / copy_gbs, 4)
     ops["fork"] = {"us": round(ms("fork") * 1e3, 2)}
     ops["evict"] = {"us": round(ms("release") * 1e3, 2)}
 
@@ -406,6 +417,8 @@ def main():
         "ops": ops,
         "roofline": roofline,
         "kernel_ms_per_step": {k: round(v[1] / K, 4) for k, v in prof.items() if v[0]},
+        "copy_reference": {"GB/s": round(copy_gbs, 1), "what": "torch device-to-device copy "
+                           "of 1 GiB (read + write bytes), same run"},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, args.seed)
