@@ -509,58 +509,65 @@ k_qkv_decode(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restr
   }
 }
 
-// Decode-size projection with the token rows staged in LDS (M <= 16 rows
-// whose padded copy fits): the x operand is read from LDS (row stride d + 8
-// elements, so the 16 rows one operand read touches fall in distinct bank
-// groups) instead of being fetched again from L2 by every wavefront, and the
-// next batch of weight loads is issued before the products of the current
-// one.  Same tiling as k_qkv_decode<1>; dynamic LDS: M * (d + 8) bf16.
+// Decode-size projection with the token rows staged in LDS (M <= 16 rows):
+// the x operand is read from LDS (row stride kc + 8 elements, so the 16 rows
+// one operand read touches fall in distinct bank groups) instead of being
+// fetched again from L2 by every wavefront, and the next batch of weight
+// loads is issued before the products of the current one.  x is staged in
+// column chunks of kc (the launcher picks the widest that lets two
+// workgroups share a CU).  Same tiling as k_qkv_decode<1>; dynamic LDS:
+// M * (kc + 8) bf16.
 constexpr int kDecU = 8;  // k-steps of 32 per load batch (two batches in flight)
 
 __global__ void __launch_bounds__(64 * kDecWaves)
 k_qkv_decode_lds(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
-                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
+                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0, int kc) {
   constexpr int FLD = kDh + 4;
   constexpr int NT = 64 * kDecWaves;
   __shared__ __attribute__((aligned(16))) float Cf[16 * FLD];
-  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][d + 8]
+  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][kc + 8]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lk = (lane >> 4) * 8;
   const int n0 = blockIdx.x * kDh;
   const int lc = blockIdx.z, l = l0 + lc;
-  const int M = a.batch * a.T, d = g.d, xld = d + 8;
+  const int M = a.batch * a.T, d = g.d, xld = kc + 8;
   const uint16_t* wl = w + (int64_t)l * w_stride;
   const uint16_t* wr = wl + (int64_t)(n0 + wave * 16 + lr) * d + lk;
-
-  // weights of the first batch, then the token rows into LDS
-  uint4 fa[kDecU], fn[kDecU];
-#pragma unroll
-  for (int u = 0; u < kDecU; ++u) fa[u] = *(const uint4*)(wr + 32 * u);
-  const int d8 = d / 8;
-  for (int i = tid; i < M * d8; i += NT) {
-    const int r = i / d8, c = i - r * d8;
-    *(uint4*)(xs + r * xld + c * 8) = *(const uint4*)(x + (int64_t)r * d + c * 8);
-  }
-  __syncthreads();
   const bool xok = lr < M;
   const uint16_t* xr = xs + (xok ? lr : 0) * xld + lk;
 
+  // weights of the first batch in flight while the first x chunk is staged
+  uint4 fa[kDecU], fn[kDecU];
+#pragma unroll
+  for (int u = 0; u < kDecU; ++u) fa[u] = *(const uint4*)(wr + 32 * u);
   floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < d; k0 += 32 * kDecU) {
-    const bool more = k0 + 32 * kDecU < d;
-    if (more) {
-#pragma unroll
-      for (int u = 0; u < kDecU; ++u) fn[u] = *(const uint4*)(wr + k0 + 32 * kDecU + 32 * u);
+  const int c8 = kc / 8;
+  for (int kc0 = 0; kc0 < d; kc0 += kc) {
+    // token rows, columns [kc0, kc0 + kc), into LDS
+    if (kc0 > 0) __syncthreads();  // the previous chunk has been read
+    for (int i = tid; i < M * c8; i += NT) {
+      const int r = i / c8, c = i - r * c8;
+      *(uint4*)(xs + r * xld + c * 8) = *(const uint4*)(x + (int64_t)r * d + kc0 + c * 8);
     }
+    __syncthreads();
+    for (int k0 = kc0; k0 < kc0 + kc; k0 += 32 * kDecU) {
+      const bool more = k0 + 32 * kDecU < d;
+      if (more) {
 #pragma unroll
-    for (int u = 0; u < kDecU; ++u) {
-      const uint4 fb = xok ? *(const uint4*)(xr + k0 + 32 * u) : make_uint4(0, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa[u]),
-                                                    __builtin_bit_cast(bf16x8v, fb), acc, 0, 0, 0);
-    }
-    if (more) {
+        for (int u = 0; u < kDecU; ++u) fn[u] = *(const uint4*)(wr + k0 + 32 * kDecU + 32 * u);
+      }
 #pragma unroll
-      for (int u = 0; u < kDecU; ++u) fa[u] = fn[u];
+      for (int u = 0; u < kDecU; ++u) {
+        const uint4 fb =
+            xok ? *(const uint4*)(xr + (k0 - kc0) + 32 * u) : make_uint4(0, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa[u]),
+                                                      __builtin_bit_cast(bf16x8v, fb), acc, 0, 0,
+                                                      0);
+      }
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < kDecU; ++u) fa[u] = fn[u];
+      }
     }
   }
   // C[16 ch x 16 tok]: lane holds channels 4 (lane / 16) + e of token lane % 16
@@ -605,11 +612,16 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
                            const AppendDesc& a, void* qbuf, int l0, int lc, hipStream_t s) {
   const int M = a.batch * a.T;
   const int N = (g.Hq + 2 * g.Hkv) * kDh;
-  const size_t x_lds = (size_t)M * (g.d + 8) * 2;
-  if (M <= 16 && g.d % (32 * kDecU) == 0 && x_lds + 16 * (kDh + 4) * 4 <= 160 * 1024) {
+  // x staged in column chunks of kc: the whole row if two workgroups still
+  // fit in a CU's LDS, else halves, quarters, ... (multiples of the batch width)
+  int kc = g.d;
+  const size_t cf_bytes = 16 * (kDh + 4) * 4;
+  while (kc % (2 * 32 * kDecU) == 0 && (size_t)M * (kc + 8) * 2 + cf_bytes > 80 * 1024) kc /= 2;
+  const size_t x_lds = (size_t)M * (kc + 8) * 2;
+  if (M <= 16 && g.d % (32 * kDecU) == 0 && x_lds + cf_bytes <= 160 * 1024) {
     dim3 grid(N / kDh, 1, lc);
     k_qkv_decode_lds<<<grid, 64 * kDecWaves, x_lds, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
-                                                         w_stride, a, (uint16_t*)qbuf, l0);
+                                                         w_stride, a, (uint16_t*)qbuf, l0, kc);
   } else if (M <= 16 && g.d % 512 == 0) {
     dim3 grid(N / kDh, 1, lc);
     k_qkv_decode<1><<<grid, 64 * kDecWaves, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
