@@ -61,6 +61,19 @@ constexpr int kXcd = 8;             // XCDs per device
 constexpr size_t kLdsMax = 160 * 1024;
 constexpr size_t kStaticLds = (size_t)kPS * 2 * kPTile * 2;
 
+// Reductions over lanes l and l ^ 32 (the two halves of a token's keys) with
+// v_permlane32_swap, which leaves v[l % 32] and v[l % 32 + 32] in every lane.
+__device__ inline float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // LDS slot permutations of a key row's 16 chunks of 16 bytes.  K rows are
 // read 16 consecutive rows at one chunk: chunk c of row r sits at slot
 // c ^ (r & 15).  V rows are read transposed, 8 consecutive rows x 4 adjacent
@@ -243,7 +256,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sacc[kt][e]);
-    mt_max = fmaxf(mt_max, __shfl_xor(mt_max, 32)) * qk_scale_log2;
+    mt_max = max_xor32(mt_max) * qk_scale_log2;
     const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     const bool moved = __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run) != 0)) != 0;
@@ -301,7 +314,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     }
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = sum_xor32(l_run);
   if (!q_valid) return;
   const float inv = 1.f / l_tot;
   const int row = seq * a.T + tq;

@@ -44,6 +44,19 @@ struct DecodeUnit {
   uint32_t mask_lo, mask_hi;
 };
 
+// Reductions over lanes l and l ^ 32 (the two halves of a token's keys) with
+// v_permlane32_swap, which leaves v[l % 32] and v[l % 32 + 32] in every lane.
+__device__ inline float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // LDS slot of chunk c of key row r: c ^ kswz(r) for K (read 16 rows at one
 // chunk), c ^ vswz(r) for V (read transposed, 8 rows x 4 adjacent chunks);
 // both spread each read over all bank groups.
@@ -290,7 +303,7 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
           sacc[rt][e] = sv;
           mx = fmaxf(mx, sv);
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * qk_scale_log2;
+        mx = max_xor32(mx) * qk_scale_log2;
         const float m_new = mx > m_run[rt] + 8.f ? mx : m_run[rt];
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
         const bool moved =
@@ -345,7 +358,7 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     // partials of this unit's query vectors for chunk c
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      const float lt = l_run[rt] + __shfl_xor(l_run[rt], 32);
+      const float lt = sum_xor32(l_run[rt]);
       if (qrow[rt] < 0) continue;
       float* pp = part + ((((int64_t)lc * b + qrow[rt]) * g.Hq + qhead[rt]) * n_chunks + c) * kPart;
 #pragma unroll
