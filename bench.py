@@ -178,9 +178,10 @@ def transfer_sweep(args, kv, torch, synth):
     x = synth.normal_torch(synth.x_key(args.seed, wl.name, 0), (nmax, d), 1.0, s.dtype, dev)
     o = torch.empty((L, nmax, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
     buf = torch.empty((nmax // B) * s.block_bytes, dtype=torch.uint8, device=dev)
+    host = torch.empty((nmax // B) * s.block_bytes, dtype=torch.uint8, pin_memory=True)
     rows = []
     for n in lengths:
-        times = {"mat": [], "pack": [], "unpack": []}
+        times = {"mat": [], "pack": [], "unpack": [], "pack_host": [], "unpack_host": []}
         for rep in range(3):
             kv.kv_profile_enable(pool.h, True)
             kv.kv_profile_read(pool.h)
@@ -189,6 +190,11 @@ def transfer_sweep(args, kv, torch, synth):
             hdr = kv.kv_pack(pool.h, st, 0, nb, buf)
             u = kv.kv_unpack(pool.h, hdr, buf)
             prof = kv.kv_profile_read(pool.h)
+            kv.kv_release(pool.h, u)
+            # the host tier: pack into pinned host memory, unpack from it
+            hdr_h = kv.kv_pack(pool.h, st, 0, nb, host)
+            u = kv.kv_unpack(pool.h, hdr_h, host)
+            prof_h = kv.kv_profile_read(pool.h)
             kv.kv_profile_enable(pool.h, False)
             kv.kv_release(pool.h, st)
             kv.kv_release(pool.h, u)
@@ -197,15 +203,24 @@ def transfer_sweep(args, kv, torch, synth):
             times["mat"].append(sum(prof[k][1] for k in ("alloc", "qkv", "attn")))
             times["pack"].append(prof["pack"][1])
             times["unpack"].append(prof["unpack"][1])
+            times["pack_host"].append(prof_h["pack"][1])
+            times["unpack_host"].append(prof_h["unpack"][1])
         t_mat = min(times["mat"]) / 1e3
         t_pack = min(times["pack"]) / 1e3
         t_unpack = min(times["unpack"]) / 1e3
         kvb = (-(-n // B)) * s.block_bytes
         fl = kv.kv_plan_transfer(cfg, n, 1.0, 0.0, 0.0, 0.0, 1.0)["prefill_flops"]
         rate = fl / t_mat
+        t_ph = min(times["pack_host"]) / 1e3
+        t_uh = min(times["unpack_host"]) / 1e3
         row = {"tokens": n, "kv_bytes": kvb, "materialize_ms": round(t_mat * 1e3, 3),
                "prefill_TFLOPs": round(rate / 1e12, 1), "pack_ms": round(t_pack * 1e3, 4),
-               "unpack_ms": round(t_unpack * 1e3, 4), "links": {}}
+               "unpack_ms": round(t_unpack * 1e3, 4),
+               "host_tier": {"pack_ms": round(t_ph * 1e3, 3), "unpack_ms": round(t_uh * 1e3, 3),
+                             "pack_GBs": round(kvb / t_ph / 1e9, 1),
+                             "unpack_GBs": round(kvb / t_uh / 1e9, 1),
+                             "reload_vs_recompute": round(t_mat / t_uh, 1)},
+               "links": {}}
         for name, bw, lat in LINKS:
             plan = kv.kv_plan_transfer(cfg, n, bw, lat, kvb / t_pack, kvb / t_unpack, rate)
             row["links"][name] = {"transfer_ms": round(plan["t_transfer"] * 1e3, 3),

@@ -160,13 +160,16 @@ kv_status kv_compose(kv_pool* pool, const kv_segment* segs, int32_t n, kv_stream
 /* KV-Transfer, source side: write logical blocks [blk_begin, blk_end) of
  * `state` to dst_dev as n_blocks * block_bytes contiguous bytes in logical
  * order (each block in the pool's block layout; slots after the state's last
- * token zero-filled) and fill *hdr_out. */
+ * token zero-filled) and fill *hdr_out.  dst_dev is device memory or pinned
+ * host memory (hipHostMalloc; the host tier of a state, written over the
+ * host link); any other pointer is KV_ERR_ARG.  16-byte aligned. */
 kv_status kv_pack(kv_pool* pool, kv_state state, int64_t blk_begin, int64_t blk_end,
                   void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream);
 
 /* KV-Transfer, destination side: check the header (KV_ERR_BAD_HEADER) and
  * compatibility (KV_ERR_INCOMPATIBLE), allocate n_blocks blocks from the free
- * ring, copy the payload and register a state at positions pos_begin .. */
+ * ring, copy the payload and register a state at positions pos_begin ..
+ * src_dev is device memory or pinned host memory (as for kv_pack). */
 kv_status kv_unpack(kv_pool* pool, const kv_pack_header* hdr, const void* src_dev,
                     size_t src_bytes, kv_stream stream, kv_state* out);
 

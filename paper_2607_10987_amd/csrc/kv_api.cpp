@@ -371,6 +371,33 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
 
 }  // namespace
 
+namespace {
+
+// Device address of a buffer the data-movement kernels read or write:
+// device memory as is, pinned host memory (hipHostMalloc) through its device
+// mapping; pageable or unknown host memory is rejected, so that no kernel is
+// ever launched on an address the GPU cannot reach.
+kv_status device_view(const void* p, const void** out) {
+  hipPointerAttribute_t a;
+  std::memset(&a, 0, sizeof(a));
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return KV_ERR_ARG;
+  }
+  if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) {
+    *out = p;
+    return KV_OK;
+  }
+  if (a.type == hipMemoryTypeHost && a.devicePointer) {
+    const ptrdiff_t off = a.hostPointer ? (const char*)p - (const char*)a.hostPointer : 0;
+    *out = (const char*)a.devicePointer + off;
+    return KV_OK;
+  }
+  return KV_ERR_ARG;
+}
+
+}  // namespace
+
 extern "C" {
 
 kv_status kv_plan_transfer(const kv_model_cfg* cfg, int64_t n_tokens, double link_bytes_per_s,
@@ -728,6 +755,8 @@ kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end
   StateRec& r = p->slots[slot];
   if (!(0 <= blk_begin && blk_begin < blk_end && blk_end <= r.nblocks)) return KV_ERR_ARG;
   if ((uintptr_t)dst_dev & 15) return KV_ERR_ARG;
+  const void* dst_view = nullptr;
+  KV_TRY(device_view(dst_dev, &dst_view));
   const kv_model_cfg& c = p->cfg;
   const int B = c.block_size;
   const PoolGeom g = p->geom();
@@ -751,8 +780,8 @@ kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end
   const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * B);
   {
     Timed t(p, KV_KERNEL_PACK, S(stream));
-    KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid, dst_dev,
-                       S(stream)));
+    KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid,
+                       const_cast<void*>(dst_view), S(stream)));
   }
   p->touch(r, true);
   *hdr_out = h;
@@ -763,6 +792,8 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
                     kv_stream stream, kv_state* out) {
   if (!p || !hdr || !src_dev || !out) return KV_ERR_ARG;
   if ((uintptr_t)src_dev & 15) return KV_ERR_ARG;
+  const void* src_view = nullptr;
+  KV_TRY(device_view(src_dev, &src_view));
   if (hdr->magic != KV_PACK_MAGIC || hdr->version != KV_PACK_VERSION) return KV_ERR_BAD_HEADER;
   const kv_model_cfg& c = p->cfg;
   if (hdr->model_id != c.model_id || !same_theta(hdr->cfg, c)) return KV_ERR_INCOMPATIBLE;
@@ -791,7 +822,7 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
   if (nt % B) r.group = p->new_group(1);
   {
     Timed t(p, KV_KERNEL_UNPACK, s);
-    KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_dev, s));
+    KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_view, s));
   }
   p->touch(r, false);
   *out = p->handle(slot);

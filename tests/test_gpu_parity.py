@@ -138,6 +138,38 @@ def test_pack_unpack_bit_exact_round_trips(gpu_available):
         tw.close()
 
 
+def test_pack_unpack_pinned_host_tier(gpu_available):
+    """Pack to / unpack from pinned host memory (the host tier of a state):
+    the same bytes as through device memory, and a round trip through the
+    host gives back the same blocks.  Pageable host memory is rejected before
+    anything is enqueued."""
+    shape = small_shape("bf16", B=4, dh=32, L=3, hq=4, hkv=2)
+    tw = Twin(shape, n_blocks=48, max_pos=128, wl="hosttier")
+    hdr, ohdr, buf, pay = tw.synthetic_transfer(5, 18, 7, tag=3)
+    u = tw.unpack(hdr, ohdr, buf, pay)
+    hdr_d, _, dev_buf, _ = tw.pack(u, 0, 5)          # device pack, checked against the oracle
+    host = torch.empty(dev_buf.numel(), dtype=torch.uint8, pin_memory=True)
+    hdr_h = kv.kv_pack(tw.gpu.h, u, 0, 5, host)
+    torch.cuda.synchronize()
+    assert torch.equal(host, dev_buf.cpu())
+    assert bytes(hdr_h) == bytes(hdr_d)
+    v = kv.kv_unpack(tw.gpu.h, hdr_h, host)
+    again = torch.empty_like(dev_buf)
+    kv.kv_pack(tw.gpu.h, v, 0, 5, again)
+    torch.cuda.synchronize()
+    assert torch.equal(again, dev_buf)
+    before = kv.kv_pool_counts(tw.gpu.h)
+    page = torch.empty(dev_buf.numel(), dtype=torch.uint8)  # pageable
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_pack(tw.gpu.h, u, 0, 5, page)
+    assert e.value.status == kv.KV_ERR_ARG
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_unpack(tw.gpu.h, hdr_h, page)
+    assert e.value.status == kv.KV_ERR_ARG
+    assert kv.kv_pool_counts(tw.gpu.h) == before
+    tw.close()
+
+
 def test_error_codes_on_device(gpu_available):
     tw = Twin(small_shape(B=2), n_blocks=4, max_pos=16, max_states=3, wl="err")
     x = torch.zeros((9, 32), dtype=torch.float32, device="cuda")
