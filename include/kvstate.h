@@ -15,7 +15,8 @@
  * - Device work is enqueued on `stream` (a hipStream_t passed as void*; NULL
  *   is the default stream).  All mutating calls on one pool must use one
  *   stream (or be ordered by the caller); concurrent calls on one pool race.
- *   kv_release and kv_evict synchronise `stream` before returning.
+ *   kv_release, kv_evict and kv_evict_truncate synchronise `stream`
+ *   before returning.
  * - The caller owns all device memory: the pool, the metadata area, the
  *   scratch area, weights, inputs, outputs and transfer buffers.  Device
  *   pointers must be 256-byte aligned.  The library owns only host-side
@@ -49,7 +50,9 @@ enum {
   KV_ERR_BUFSIZE = -6,      /* caller buffer too small */
   KV_ERR_CAPACITY = -7,     /* catalog full or positions beyond max_pos */
   KV_ERR_HIP = -8,          /* HIP runtime error */
-  KV_ERR_INTERNAL = -9      /* device consistency check failed */
+  KV_ERR_INTERNAL = -9,     /* device consistency check failed */
+  KV_ERR_CHECKSUM = -10,    /* payload does not match the header's checksum */
+  KV_ERR_IO = -11           /* checkpoint file could not be opened, read or written */
 };
 
 enum { KV_DTYPE_F32 = 0, KV_DTYPE_BF16 = 1 };
@@ -90,7 +93,8 @@ typedef struct {
 } kv_segment;
 
 #define KV_PACK_MAGIC 0x5453564Bu
-#define KV_PACK_VERSION 1u
+#define KV_PACK_VERSION 2u
+#define KV_PACK_CHECKSUM 1u /* kv_pack_header.flags: checksum[] is set */
 
 /* Metadata descriptor sent beside a packed payload (KV-Transfer algorithm:
  * metadata travels separately from the raw block buffers).  Plain old data. */
@@ -106,6 +110,13 @@ typedef struct {
   uint64_t payload_bytes;
   uint64_t lineage;      /* source state's lineage word */
   int64_t src_state_id;  /* source state's id */
+  uint32_t flags;        /* KV_PACK_CHECKSUM or 0; other bits invalid */
+  uint32_t reserved;     /* 0 */
+  /* With KV_PACK_CHECKSUM: payload read as little-endian uint32 words
+   * w_0 .. w_{N-1}, checksum[0] = sum of w_i and checksum[1] = sum of
+   * (i + 1) * w_i, both mod 2^64 (a position-weighted sum: any single changed
+   * word and any exchange of two unequal words change it). */
+  uint64_t checksum[2];
 } kv_pack_header;
 
 /* Sizes of the caller-provided device areas for a pool of n_blocks blocks.
@@ -166,12 +177,38 @@ kv_status kv_compose(kv_pool* pool, const kv_segment* segs, int32_t n, kv_stream
 kv_status kv_pack(kv_pool* pool, kv_state state, int64_t blk_begin, int64_t blk_end,
                   void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream);
 
+/* kv_pack with the payload checksum computed in the same pass over the bytes
+ * (fused into the copy kernel) and stored in hdr_out->checksum, with
+ * KV_PACK_CHECKSUM in hdr_out->flags.  Synchronises `stream`. */
+kv_status kv_pack_checked(kv_pool* pool, kv_state state, int64_t blk_begin, int64_t blk_end,
+                          void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out,
+                          kv_stream stream);
+
 /* KV-Transfer, destination side: check the header (KV_ERR_BAD_HEADER) and
  * compatibility (KV_ERR_INCOMPATIBLE), allocate n_blocks blocks from the free
  * ring, copy the payload and register a state at positions pos_begin ..
- * src_dev is device memory or pinned host memory (as for kv_pack). */
+ * src_dev is device memory or pinned host memory (as for kv_pack).
+ * With KV_PACK_CHECKSUM in hdr->flags the copy also computes the payload's
+ * checksum and the call synchronises `stream`; on a mismatch the new blocks
+ * go back to the tail of the free ring (logical order), the state id drawn
+ * for the state is not reused, and the result is KV_ERR_CHECKSUM. */
 kv_status kv_unpack(kv_pool* pool, const kv_pack_header* hdr, const void* src_dev,
                     size_t src_bytes, kv_stream stream, kv_state* out);
+
+/* File checkpoint of a state (persistence of the host tier): the header of a
+ * checksummed pack of all of the state's blocks, then its payload, written
+ * through a pinned host staging buffer of at most 64 MiB (whole blocks, at
+ * least one), so any state size works.  The state counts as used (like
+ * kv_pack).  KV_ERR_IO if the file cannot be written.  Synchronous. */
+kv_status kv_checkpoint_save(kv_pool* pool, kv_state state, const char* path,
+                             kv_stream stream);
+
+/* Restore a file written by kv_checkpoint_save as a new state, with the
+ * checks and the result of kv_unpack (header, compatibility, capacity, then
+ * the checksum over the whole payload: KV_ERR_CHECKSUM with the same roll
+ * back).  KV_ERR_IO if the file cannot be read or is shorter than its header
+ * says.  Synchronous. */
+kv_status kv_checkpoint_load(kv_pool* pool, const char* path, kv_stream stream, kv_state* out);
 
 /* KV-Resume over a batch (append-prefill when T > 1, decode when T = 1): for
  * each state in order, copy-on-write a shared partial tail block, allocate the
@@ -188,6 +225,19 @@ kv_status kv_attend(kv_pool* pool, const kv_state* states, int32_t batch, const 
  * number of states evicted. */
 kv_status kv_evict(kv_pool* pool, int64_t max_allocated_blocks, double alpha, double beta,
                    double gamma, kv_stream stream, int32_t* n_evicted);
+
+/* KV-Evict, the branch for states that share blocks: candidates in the order
+ * of kv_evict, while allocated blocks > max_allocated_blocks; a candidate
+ * keeps the leading blocks in front of its first block that no other state
+ * references (refcount 1) and gives up every block from there on (freed if
+ * unshared, else decremented), its token count becoming those whole blocks'
+ * (truncation to the shared prefix: only the continuation is lost and can be
+ * recomputed).  A candidate whose first block is unshared is evicted whole;
+ * one with no unshared block is left unchanged.  Synchronous.
+ * *n_evicted / *n_truncated: states evicted whole / truncated. */
+kv_status kv_evict_truncate(kv_pool* pool, int64_t max_allocated_blocks, double alpha,
+                            double beta, double gamma, kv_stream stream, int32_t* n_evicted,
+                            int32_t* n_truncated);
 
 /* Drop a state's block references (blocks reaching refcount 0 return to the
  * tail of the free ring, in logical order).  Synchronous. */

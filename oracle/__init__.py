@@ -14,6 +14,7 @@ Modules
              catalog, and the seven operators (materialize, fork, attend,
              compose, pack, unpack, evict) plus release and pin
   policy     the transfer-vs-recompute decision of the scheduling rule
+  checksum   the payload checksum of checked packs and file checkpoints
 
 Operator semantics follow the paper's stateful-operator section (state object
 S_KV = (M, Theta, B, Pi, Lambda, Gamma), Compat predicate, operator
@@ -28,3 +29,4 @@ from .model import project_qkv, project_kv, project_q, split_w  # noqa: F401
 from .pool import (OraclePool, OracleError, Status, Lineage,  # noqa: F401
                    PACK_MAGIC, PACK_VERSION)
 from .policy import kv_bytes, prefill_flops, plan_transfer  # noqa: F401
+from .checksum import payload_checksum  # noqa: F401

@@ -46,7 +46,13 @@ Readings taken where the paper is silent (each is listed in the design notes):
 * a logical clock advances once per state touched (inputs in argument order,
   then outputs); eviction orders unpinned active states by (score, state_id)
   with age = clock - last_access, size = blocks in the table, reuse = times
-  the state was an operator input.
+  the state was an operator input;
+* KV-Evict's branch for a state whose blocks are shared (give up only the
+  unshared continuation) is offered as ``evict_truncate``: the victim keeps
+  the blocks in front of its first unshared one, whole blocks only;
+* a checked transfer (header flag) is verified against the payload checksum
+  of ``checksum.py`` after allocation; a mismatch returns the blocks to the
+  ring and fails.
 """
 from __future__ import annotations
 
@@ -59,9 +65,11 @@ import numpy as np
 from .attention import causal_gqa_attention
 from .model import project_qkv
 from .rope import apply_rope, rerotate
+from .checksum import payload_checksum
 
 PACK_MAGIC = 0x5453564B          # "KVST" read as a little-endian uint32
-PACK_VERSION = 1
+PACK_VERSION = 2
+PACK_CHECKSUM = 1
 NO_PARENT = 0xFFFFFFFF
 MAX_SEGMENTS = 64
 MAX_BATCH = 64
@@ -78,6 +86,8 @@ class Status(IntEnum):
     CAPACITY = -7
     HIP = -8
     INTERNAL = -9
+    CHECKSUM = -10
+    IO = -11
 
 
 class Lineage(IntEnum):
@@ -473,7 +483,7 @@ class OraclePool:
                    n_tokens=min(st.n, b1 * s.block_size) - b0 * s.block_size,
                    blk_begin=b0, n_blocks=nblk, block_bytes=s.block_bytes,
                    payload_bytes=nblk * s.block_bytes, lineage=st.lineage,
-                   src_state_id=st.sid)
+                   src_state_id=st.sid, flags=0, checksum=(0, 0))
         payload = None
         if self.store_kv:
             payload = np.zeros((nblk,) + self.kv.shape[1:])
@@ -483,11 +493,20 @@ class OraclePool:
         self._touch(st, as_input=True)
         return hdr, payload
 
-    def unpack(self, hdr: dict, payload=None, src_bytes: int = None):
-        """Transfer destination side: check the header, allocate, copy, register."""
+    def unpack(self, hdr: dict, payload=None, src_bytes: int = None, raw: bytes = None):
+        """Transfer destination side: check the header, allocate, copy, register.
+
+        A header flagged with a checksum is verified against ``raw``, the
+        payload's bytes, after the blocks are allocated (the copy and the
+        check are one pass on a device): on a mismatch the blocks go back to
+        the ring tail in logical order, the drawn state id stays used, and
+        the call fails with CHECKSUM.
+        """
         s = self.shape
         if hdr.get("magic") != PACK_MAGIC or hdr.get("version") != PACK_VERSION:
             raise OracleError(Status.BAD_HEADER, "magic/version")
+        if hdr.get("flags", 0) & ~PACK_CHECKSUM:
+            raise OracleError(Status.BAD_HEADER, "unknown flags")
         if hdr["model_id"] != s.model_id or tuple(hdr["compat"]) != s.compat_key():
             raise OracleError(Status.INCOMPATIBLE, "model or configuration differs")
         nb, nt = hdr["n_blocks"], hdr["n_tokens"]
@@ -507,6 +526,13 @@ class OraclePool:
                              lineage_word(Lineage.TRANSFER, hdr["src_state_id"]))
         st.table = self._alloc(nb)
         st.n = int(nt)
+        if hdr.get("flags", 0) & PACK_CHECKSUM:
+            if raw is None:
+                raise OracleError(Status.ARG, "checked header without payload bytes")
+            if payload_checksum(raw) != tuple(hdr["checksum"]):
+                self._drop_refs(st)
+                st.status = "RELEASED"
+                raise OracleError(Status.CHECKSUM, "payload does not match its checksum")
         if self.store_kv and payload is not None:
             for i, b in enumerate(st.table):
                 self.kv[b] = payload[i]
@@ -541,6 +567,41 @@ class OraclePool:
             st.status = "EVICTED"
             n += 1
         return n
+
+    def evict_truncate(self, max_allocated: int, alpha=0.0, beta=0.0, gamma=1.0):
+        """KV-Evict, the branch for a state that shares blocks (KV-Evict
+        algorithm, the alternative to freeing the whole state): a victim keeps
+        the prefix of its table in front of its first unshared block
+        (refcount 1) and drops every block from there on, so only its
+        continuation is given up; its token count becomes that prefix's
+        (whole blocks).  A victim with no shared leading block is evicted
+        whole; one with no unshared block frees nothing and is left as it is.
+        Victims in score order while allocated > budget.  Returns
+        (states evicted, states truncated)."""
+        if max_allocated < 0:
+            raise OracleError(Status.ARG, "negative budget")
+        n_ev = n_tr = 0
+        B = self.shape.block_size
+        for st in self.eviction_order(alpha, beta, gamma):
+            if self.allocated() <= max_allocated:
+                break
+            j = next((i for i, b in enumerate(st.table) if self.refcount[b] == 1),
+                     len(st.table))
+            if j == len(st.table):
+                continue
+            if j == 0:
+                self._drop_refs(st)
+                st.status = "EVICTED"
+                n_ev += 1
+                continue
+            for b in st.table[j:]:
+                self.refcount[b] -= 1
+                if self.refcount[b] == 0:
+                    self._free(b)
+            st.table = st.table[:j]
+            st.n = j * B
+            n_tr += 1
+        return n_ev, n_tr
 
     # ------------------------------------------------------------ queries
 

@@ -10,6 +10,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -45,7 +46,7 @@ uint64_t lineage_word(uint64_t kind, uint64_t parent, uint64_t j) {
 }
 
 struct MetaLayout {
-  size_t hdr, rc, ring, tables, rope_cos, rope_sin, cow, cmd, total;
+  size_t hdr, rc, ring, tables, rope_cos, rope_sin, cow, cmd, csum, total;
 };
 
 MetaLayout meta_layout(const kv_model_cfg& c, int64_t P) {
@@ -67,7 +68,9 @@ MetaLayout meta_layout(const kv_model_cfg& c, int64_t P) {
   m.cow = off;
   off = align256(off + KV_MAX_BATCH * sizeof(int2));
   m.cmd = off;
-  off = align256(off + (size_t)c.max_states * 2 * 4);
+  off = align256(off + (size_t)c.max_states * 3 * 4);  // candidates, then kept counts
+  m.csum = off;
+  off = align256(off + (size_t)(kSumSlots + 1) * 2 * 8);  // slots, then the result
   m.total = off;
   return m;
 }
@@ -94,6 +97,9 @@ kv_status check_cfg(const kv_model_cfg* c) {
 
 }  // namespace
 
+static_assert(sizeof(kv_model_cfg) == 56, "kv_model_cfg layout");
+static_assert(sizeof(kv_pack_header) == 160, "kv_pack_header layout");
+
 struct kv_pool {
   kv_model_cfg cfg;
   int64_t P = 0;
@@ -111,6 +117,7 @@ struct kv_pool {
   float* rope_sin = nullptr;
   int2* cow = nullptr;
   int32_t* cmd = nullptr;
+  unsigned long long* csum = nullptr;  // kSumSlots (s1, s2) slots, then the result pair
   int64_t head = 0, tail = 0;  // exact mirror of the device counters
   std::vector<StateRec> slots;
   int64_t next_sid = 0;
@@ -277,24 +284,34 @@ kv_status run_alloc(kv_pool* p, const AllocArgs& a, hipStream_t s) {
 }
 
 // Release states (slot, nblocks) in order; synchronous.  max_alloc < 0 releases
-// all of them.  Returns the number released.
+// all of them.  Returns the number of candidates visited.  With kept != null,
+// candidates are truncated to their shared prefix instead (see k_release) and
+// kept[i] receives the blocks candidate i keeps, for the visited ones.
 kv_status run_release(kv_pool* p, const std::vector<int32_t>& cand, int64_t max_alloc,
-                      hipStream_t s, int32_t* n_done) {
+                      hipStream_t s, int32_t* n_done, std::vector<int32_t>* kept = nullptr) {
   const int32_t n = (int32_t)(cand.size() / 2);
   *n_done = 0;
   if (n == 0) return KV_OK;
+  int32_t* kept_dev = p->cmd + 2 * (size_t)p->cfg.max_states;
   KV_HIP(hipMemcpyAsync(p->cmd, cand.data(), cand.size() * 4, hipMemcpyHostToDevice, s));
   {
     Timed t(p, KV_KERNEL_RELEASE, s);
     KV_HIP(launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
-                          p->cmd, n, max_alloc, p->head, p->tail, s));
+                          p->cmd, n, max_alloc, p->head, p->tail, kept ? 1 : 0,
+                          kept ? kept_dev : nullptr, s));
   }
   DevHeader h;
   KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
+  if (kept) {
+    kept->assign((size_t)n, -1);
+    KV_HIP(hipMemcpyAsync(kept->data(), kept_dev, (size_t)n * 4, hipMemcpyDeviceToHost, s));
+  }
   KV_HIP(hipStreamSynchronize(s));
-  if (h.status != 0 || h.head != p->head) return KV_ERR_INTERNAL;
+  if (h.status != 0 || h.head != p->head || h.n_evicted < 0 || h.n_evicted > n)
+    return KV_ERR_INTERNAL;
   p->tail = h.tail;
   *n_done = h.n_evicted;
+  if (kept) kept->resize((size_t)h.n_evicted);
   return KV_OK;
 }
 
@@ -396,6 +413,153 @@ kv_status device_view(const void* p, const void** out) {
   return KV_ERR_ARG;
 }
 
+
+// Unpinned live states in eviction order: score = alpha*reuse - beta*size -
+// gamma*age ascending, ties by state id.  Returns (slot, n_blocks) pairs.
+std::vector<int32_t> eviction_candidates(const kv_pool* p, double alpha, double beta,
+                                         double gamma) {
+  struct Cand {
+    double score;
+    int64_t sid;
+    int32_t slot;
+  };
+  std::vector<Cand> cs;
+  for (size_t i = 0; i < p->slots.size(); ++i) {
+    const StateRec& r = p->slots[i];
+    if (r.status != ST_ACTIVE || r.pinned) continue;
+    const double age = (double)(p->clock - r.last_access);
+    const double score = (alpha * (double)r.reuse - beta * (double)r.nblocks) - gamma * age;
+    cs.push_back({score, r.sid, (int32_t)i});
+  }
+  std::sort(cs.begin(), cs.end(), [](const Cand& a, const Cand& b) {
+    return a.score < b.score || (a.score == b.score && a.sid < b.sid);
+  });
+  std::vector<int32_t> cand;
+  for (const auto& c : cs) {
+    cand.push_back(c.slot);
+    cand.push_back((int32_t)p->slots[c.slot].nblocks);
+  }
+  return cand;
+}
+
+// Header of a pack of blocks [b0, b1) of state r (checksum fields zero).
+kv_pack_header make_header(const kv_pool* p, const StateRec& r, int64_t b0, int64_t b1) {
+  const kv_model_cfg& c = p->cfg;
+  const int B = c.block_size;
+  const uint64_t block_bytes = (uint64_t)p->geom().block_elems * elt_bytes(c);
+  kv_pack_header h;
+  std::memset(&h, 0, sizeof(h));
+  h.magic = KV_PACK_MAGIC;
+  h.version = KV_PACK_VERSION;
+  h.model_id = c.model_id;
+  h.cfg = c;
+  h.pos_begin = r.pos0 + b0 * B;
+  h.n_tokens = std::min<int64_t>(r.n, b1 * B) - b0 * B;
+  h.blk_begin = b0;
+  h.n_blocks = b1 - b0;
+  h.block_bytes = block_bytes;
+  h.payload_bytes = (b1 - b0) * block_bytes;
+  h.lineage = r.lineage;
+  h.src_state_id = r.sid;
+  return h;
+}
+
+// The receiving side's checks of a header, in the order kv_unpack documents.
+kv_status check_header(const kv_pool* p, const kv_pack_header* hdr) {
+  if (hdr->magic != KV_PACK_MAGIC || hdr->version != KV_PACK_VERSION) return KV_ERR_BAD_HEADER;
+  if ((hdr->flags & ~KV_PACK_CHECKSUM) != 0 || hdr->reserved != 0) return KV_ERR_BAD_HEADER;
+  const kv_model_cfg& c = p->cfg;
+  if (hdr->model_id != c.model_id || !same_theta(hdr->cfg, c)) return KV_ERR_INCOMPATIBLE;
+  const int B = c.block_size;
+  const uint64_t block_bytes = (uint64_t)p->geom().block_elems * elt_bytes(c);
+  const int64_t nb = hdr->n_blocks, nt = hdr->n_tokens;
+  if (nb < 1 || !((nb - 1) * B < nt && nt <= nb * B) || hdr->block_bytes != block_bytes ||
+      hdr->payload_bytes != nb * block_bytes || hdr->pos_begin < 0)
+    return KV_ERR_BAD_HEADER;
+  return KV_OK;
+}
+
+// Register a state for a checked header and allocate its blocks (the
+// destination side of a transfer before any byte is copied).
+kv_status open_transfer(kv_pool* p, const kv_pack_header* hdr, hipStream_t s, int32_t* slot_out) {
+  const kv_model_cfg& c = p->cfg;
+  const int64_t nb = hdr->n_blocks, nt = hdr->n_tokens;
+  if (hdr->pos_begin + nt > c.max_pos) return KV_ERR_CAPACITY;
+  const int32_t slot = p->take_slot();
+  if (slot < 0) return KV_ERR_CAPACITY;
+  if (nb > p->free_blocks()) return KV_ERR_OOM;
+  StateRec& r = p->open_state(slot, hdr->pos_begin, nt, nb,
+                              lineage_word(KV_LINEAGE_TRANSFER, (uint64_t)hdr->src_state_id, 0));
+  AllocArgs aa;
+  std::memset(&aa, 0, sizeof(aa));
+  aa.n_req = 1;
+  aa.req[0].slot = slot;
+  aa.req[0].first = 0;
+  aa.req[0].count = (int32_t)nb;
+  KV_TRY(run_alloc(p, aa, s));
+  if (nt % c.block_size) r.group = p->new_group(1);
+  *slot_out = slot;
+  return KV_OK;
+}
+
+// Undo open_transfer after a failed copy: the blocks return to the free ring,
+// the state is not registered (its id stays used).
+kv_status abort_transfer(kv_pool* p, int32_t slot, hipStream_t s) {
+  StateRec& r = p->slots[slot];
+  std::vector<int32_t> cand = {slot, (int32_t)r.nblocks};
+  int32_t n = 0;
+  KV_TRY(run_release(p, cand, -1, s, &n));
+  p->leave_group(r);
+  r.status = ST_RELEASED;
+  return KV_OK;
+}
+
+// Clear the checksum slots (the folding kernel clears what it reads; its
+// result is overwritten by csum_end).
+kv_status csum_begin(kv_pool* p, hipStream_t s) {
+  KV_HIP(launch_csum_final(p->csum, p->csum + 2 * kSumSlots, s));
+  return KV_OK;
+}
+
+// Fold the slots into (s1, s2), clear them, synchronise, return the pair.
+kv_status csum_end(kv_pool* p, hipStream_t s, uint64_t out[2]) {
+  unsigned long long* res = p->csum + 2 * kSumSlots;
+  KV_HIP(launch_csum_final(p->csum, res, s));
+  unsigned long long h[2];
+  KV_HIP(hipMemcpyAsync(h, res, sizeof(h), hipMemcpyDeviceToHost, s));
+  KV_HIP(hipStreamSynchronize(s));
+  out[0] = h[0];
+  out[1] = h[1];
+  return KV_OK;
+}
+
+// Pinned host staging buffer of whole blocks, released on scope exit.
+struct Staging {
+  void* host = nullptr;
+  const void* dev = nullptr;
+  int64_t blocks = 0;
+  ~Staging() {
+    if (host) (void)hipHostFree(host);
+  }
+  kv_status alloc(int64_t want_blocks, uint64_t block_bytes) {
+    const int64_t cap = std::max<int64_t>(1, (int64_t)((64ull << 20) / block_bytes));
+    blocks = std::min(want_blocks, cap);
+    if (hipHostMalloc(&host, (size_t)(blocks * block_bytes), hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      host = nullptr;
+      return KV_ERR_HIP;
+    }
+    return device_view(host, &dev);
+  }
+};
+
+struct File {
+  FILE* f = nullptr;
+  ~File() {
+    if (f) std::fclose(f);
+  }
+};
+
 }  // namespace
 
 extern "C" {
@@ -441,6 +605,8 @@ const char* kv_strerror(kv_status st) {
     case KV_ERR_CAPACITY: return "KV_ERR_CAPACITY";
     case KV_ERR_HIP: return "KV_ERR_HIP";
     case KV_ERR_INTERNAL: return "KV_ERR_INTERNAL";
+    case KV_ERR_CHECKSUM: return "KV_ERR_CHECKSUM";
+    case KV_ERR_IO: return "KV_ERR_IO";
     default: return "KV_ERR_UNKNOWN";
   }
 }
@@ -500,6 +666,7 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   p->rope_sin = (float*)(p->meta + p->ml.rope_sin);
   p->cow = (int2*)(p->meta + p->ml.cow);
   p->cmd = (int32_t*)(p->meta + p->ml.cmd);
+  p->csum = (unsigned long long*)(p->meta + p->ml.csum);
   p->head = 0;
   p->tail = n_blocks;
   p->slots.resize(cfg->max_states);
@@ -747,8 +914,9 @@ kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream st
   return KV_OK;
 }
 
-kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end, void* dst_dev,
-                  size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream) {
+static kv_status pack_impl(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end,
+                           void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out,
+                           kv_stream stream, bool checked) {
   if (!p || !dst_dev || !hdr_out) return KV_ERR_ARG;
   int32_t slot;
   KV_TRY(p->lookup(state, &slot));
@@ -758,34 +926,38 @@ kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end
   const void* dst_view = nullptr;
   KV_TRY(device_view(dst_dev, &dst_view));
   const kv_model_cfg& c = p->cfg;
-  const int B = c.block_size;
-  const PoolGeom g = p->geom();
-  const uint64_t block_bytes = (uint64_t)g.block_elems * elt_bytes(c);
-  const int64_t nblk = blk_end - blk_begin;
-  if (dst_bytes < nblk * block_bytes) return KV_ERR_BUFSIZE;
-  kv_pack_header h;
-  std::memset(&h, 0, sizeof(h));
-  h.magic = KV_PACK_MAGIC;
-  h.version = KV_PACK_VERSION;
-  h.model_id = c.model_id;
-  h.cfg = c;
-  h.pos_begin = r.pos0 + blk_begin * B;
-  h.n_tokens = std::min<int64_t>(r.n, blk_end * B) - blk_begin * B;
-  h.blk_begin = blk_begin;
-  h.n_blocks = nblk;
-  h.block_bytes = block_bytes;
-  h.payload_bytes = nblk * block_bytes;
-  h.lineage = r.lineage;
-  h.src_state_id = r.sid;
-  const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * B);
+  kv_pack_header h = make_header(p, r, blk_begin, blk_end);
+  if (dst_bytes < h.payload_bytes) return KV_ERR_BUFSIZE;
+  const int64_t nblk = h.n_blocks;
+  const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * c.block_size);
+  const hipStream_t s = S(stream);
+  if (checked) KV_TRY(csum_begin(p, s));
   {
-    Timed t(p, KV_KERNEL_PACK, S(stream));
-    KV_HIP(launch_pack(g, c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid,
-                       const_cast<void*>(dst_view), S(stream)));
+    Timed t(p, KV_KERNEL_PACK, s);
+    KV_HIP(launch_pack(p->geom(), c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid,
+                       const_cast<void*>(dst_view), checked ? p->csum : nullptr, 0, s));
+  }
+  if (checked) {
+    uint64_t sum[2];
+    KV_TRY(csum_end(p, s, sum));
+    h.flags = KV_PACK_CHECKSUM;
+    h.checksum[0] = sum[0];
+    h.checksum[1] = sum[1];
   }
   p->touch(r, true);
   *hdr_out = h;
   return KV_OK;
+}
+
+kv_status kv_pack(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end, void* dst_dev,
+                  size_t dst_bytes, kv_pack_header* hdr_out, kv_stream stream) {
+  return pack_impl(p, state, blk_begin, blk_end, dst_dev, dst_bytes, hdr_out, stream, false);
+}
+
+kv_status kv_pack_checked(kv_pool* p, kv_state state, int64_t blk_begin, int64_t blk_end,
+                          void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out,
+                          kv_stream stream) {
+  return pack_impl(p, state, blk_begin, blk_end, dst_dev, dst_bytes, hdr_out, stream, true);
 }
 
 kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, size_t src_bytes,
@@ -794,37 +966,119 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
   if ((uintptr_t)src_dev & 15) return KV_ERR_ARG;
   const void* src_view = nullptr;
   KV_TRY(device_view(src_dev, &src_view));
-  if (hdr->magic != KV_PACK_MAGIC || hdr->version != KV_PACK_VERSION) return KV_ERR_BAD_HEADER;
-  const kv_model_cfg& c = p->cfg;
-  if (hdr->model_id != c.model_id || !same_theta(hdr->cfg, c)) return KV_ERR_INCOMPATIBLE;
-  const int B = c.block_size;
-  const PoolGeom g = p->geom();
-  const uint64_t block_bytes = (uint64_t)g.block_elems * elt_bytes(c);
-  const int64_t nb = hdr->n_blocks, nt = hdr->n_tokens;
-  if (nb < 1 || !((nb - 1) * B < nt && nt <= nb * B) || hdr->block_bytes != block_bytes ||
-      hdr->payload_bytes != nb * block_bytes || hdr->pos_begin < 0)
-    return KV_ERR_BAD_HEADER;
+  KV_TRY(check_header(p, hdr));
   if (src_bytes < hdr->payload_bytes) return KV_ERR_BUFSIZE;
-  if (hdr->pos_begin + nt > c.max_pos) return KV_ERR_CAPACITY;
-  const int32_t slot = p->take_slot();
-  if (slot < 0) return KV_ERR_CAPACITY;
-  if (nb > p->free_blocks()) return KV_ERR_OOM;
-  StateRec& r = p->open_state(slot, hdr->pos_begin, nt, nb,
-                              lineage_word(KV_LINEAGE_TRANSFER, (uint64_t)hdr->src_state_id, 0));
   const hipStream_t s = S(stream);
-  AllocArgs aa;
-  std::memset(&aa, 0, sizeof(aa));
-  aa.n_req = 1;
-  aa.req[0].slot = slot;
-  aa.req[0].first = 0;
-  aa.req[0].count = (int32_t)nb;
-  KV_TRY(run_alloc(p, aa, s));
-  if (nt % B) r.group = p->new_group(1);
+  const bool checked = (hdr->flags & KV_PACK_CHECKSUM) != 0;
+  int32_t slot;
+  KV_TRY(open_transfer(p, hdr, s, &slot));
+  if (checked) KV_TRY(csum_begin(p, s));
   {
     Timed t(p, KV_KERNEL_UNPACK, s);
-    KV_HIP(launch_unpack(g, c.dtype, p->trow(slot), (int32_t)nb, src_view, s));
+    KV_HIP(launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot), (int32_t)hdr->n_blocks, src_view,
+                         checked ? p->csum : nullptr, 0, s));
   }
+  if (checked) {
+    uint64_t sum[2];
+    KV_TRY(csum_end(p, s, sum));
+    if (sum[0] != hdr->checksum[0] || sum[1] != hdr->checksum[1]) {
+      KV_TRY(abort_transfer(p, slot, s));
+      return KV_ERR_CHECKSUM;
+    }
+  }
+  StateRec& r = p->slots[slot];
   p->touch(r, false);
+  *out = p->handle(slot);
+  return KV_OK;
+}
+
+kv_status kv_checkpoint_save(kv_pool* p, kv_state state, const char* path, kv_stream stream) {
+  if (!p || !path) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  StateRec& r = p->slots[slot];
+  const kv_model_cfg& c = p->cfg;
+  kv_pack_header h = make_header(p, r, 0, r.nblocks);
+  const hipStream_t s = S(stream);
+  Staging st;
+  KV_TRY(st.alloc(h.n_blocks, h.block_bytes));
+  File f;
+  f.f = std::fopen(path, "wb");
+  if (!f.f) return KV_ERR_IO;
+  kv_pack_header blank;
+  std::memset(&blank, 0, sizeof(blank));
+  if (std::fwrite(&blank, sizeof(blank), 1, f.f) != 1) return KV_ERR_IO;
+  KV_TRY(csum_begin(p, s));
+  for (int64_t b = 0; b < h.n_blocks; b += st.blocks) {
+    const int64_t k = std::min(st.blocks, h.n_blocks - b);
+    const int32_t last_valid =
+        b + k == h.n_blocks ? (int32_t)(h.n_tokens - (h.n_blocks - 1) * c.block_size)
+                            : c.block_size;
+    {
+      Timed t(p, KV_KERNEL_PACK, s);
+      KV_HIP(launch_pack(p->geom(), c.dtype, p->trow(slot), b, (int32_t)k, last_valid,
+                         const_cast<void*>(st.dev), p->csum,
+                         (int64_t)(b * h.block_bytes / 16), s));
+    }
+    KV_HIP(hipStreamSynchronize(s));
+    if (std::fwrite(st.host, (size_t)(k * h.block_bytes), 1, f.f) != 1) {
+      KV_TRY(csum_begin(p, s));
+      return KV_ERR_IO;
+    }
+  }
+  uint64_t sum[2];
+  KV_TRY(csum_end(p, s, sum));
+  h.flags = KV_PACK_CHECKSUM;
+  h.checksum[0] = sum[0];
+  h.checksum[1] = sum[1];
+  if (std::fseek(f.f, 0, SEEK_SET) != 0 || std::fwrite(&h, sizeof(h), 1, f.f) != 1)
+    return KV_ERR_IO;
+  const int rc = std::fclose(f.f);
+  f.f = nullptr;
+  if (rc != 0) return KV_ERR_IO;
+  p->touch(r, true);
+  return KV_OK;
+}
+
+kv_status kv_checkpoint_load(kv_pool* p, const char* path, kv_stream stream, kv_state* out) {
+  if (!p || !path || !out) return KV_ERR_ARG;
+  File f;
+  f.f = std::fopen(path, "rb");
+  if (!f.f) return KV_ERR_IO;
+  kv_pack_header h;
+  if (std::fread(&h, sizeof(h), 1, f.f) != 1) return KV_ERR_IO;
+  KV_TRY(check_header(p, &h));
+  if (!(h.flags & KV_PACK_CHECKSUM)) return KV_ERR_BAD_HEADER;
+  if (std::fseek(f.f, 0, SEEK_END) != 0) return KV_ERR_IO;
+  const long size = std::ftell(f.f);
+  if (size < 0 || (uint64_t)size < sizeof(h) + h.payload_bytes) return KV_ERR_IO;
+  if (std::fseek(f.f, (long)sizeof(h), SEEK_SET) != 0) return KV_ERR_IO;
+  const hipStream_t s = S(stream);
+  Staging st;
+  KV_TRY(st.alloc(h.n_blocks, h.block_bytes));
+  int32_t slot;
+  KV_TRY(open_transfer(p, &h, s, &slot));
+  KV_TRY(csum_begin(p, s));
+  for (int64_t b = 0; b < h.n_blocks; b += st.blocks) {
+    const int64_t k = std::min(st.blocks, h.n_blocks - b);
+    // the previous chunk's kernel has finished reading the staging buffer
+    KV_HIP(hipStreamSynchronize(s));
+    if (std::fread(st.host, (size_t)(k * h.block_bytes), 1, f.f) != 1) {
+      KV_TRY(abort_transfer(p, slot, s));
+      KV_TRY(csum_begin(p, s));
+      return KV_ERR_IO;
+    }
+    Timed t(p, KV_KERNEL_UNPACK, s);
+    KV_HIP(launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot) + b, (int32_t)k, st.dev, p->csum,
+                         (int64_t)(b * h.block_bytes / 16), s));
+  }
+  uint64_t sum[2];
+  KV_TRY(csum_end(p, s, sum));
+  if (sum[0] != h.checksum[0] || sum[1] != h.checksum[1]) {
+    KV_TRY(abort_transfer(p, slot, s));
+    return KV_ERR_CHECKSUM;
+  }
+  p->touch(p->slots[slot], false);
   *out = p->handle(slot);
   return KV_OK;
 }
@@ -854,35 +1108,43 @@ kv_status kv_evict(kv_pool* p, int64_t max_allocated_blocks, double alpha, doubl
                    double gamma, kv_stream stream, int32_t* n_evicted) {
   if (!p || !n_evicted || max_allocated_blocks < 0) return KV_ERR_ARG;
   *n_evicted = 0;
-  struct Cand {
-    double score;
-    int64_t sid;
-    int32_t slot;
-  };
-  std::vector<Cand> cs;
-  for (size_t i = 0; i < p->slots.size(); ++i) {
-    const StateRec& r = p->slots[i];
-    if (r.status != ST_ACTIVE || r.pinned) continue;
-    const double age = (double)(p->clock - r.last_access);
-    const double score = (alpha * (double)r.reuse - beta * (double)r.nblocks) - gamma * age;
-    cs.push_back({score, r.sid, (int32_t)i});
-  }
-  std::sort(cs.begin(), cs.end(), [](const Cand& a, const Cand& b) {
-    return a.score < b.score || (a.score == b.score && a.sid < b.sid);
-  });
-  std::vector<int32_t> cand;
-  for (const auto& c : cs) {
-    cand.push_back(c.slot);
-    cand.push_back((int32_t)p->slots[c.slot].nblocks);
-  }
+  const std::vector<int32_t> cand = eviction_candidates(p, alpha, beta, gamma);
   int32_t n = 0;
   KV_TRY(run_release(p, cand, max_allocated_blocks, S(stream), &n));
   for (int i = 0; i < n; ++i) {
-    StateRec& r = p->slots[cs[i].slot];
+    StateRec& r = p->slots[cand[2 * i]];
     p->leave_group(r);
     r.status = ST_EVICTED;
   }
   *n_evicted = n;
+  return KV_OK;
+}
+
+kv_status kv_evict_truncate(kv_pool* p, int64_t max_allocated_blocks, double alpha, double beta,
+                            double gamma, kv_stream stream, int32_t* n_evicted,
+                            int32_t* n_truncated) {
+  if (!p || !n_evicted || !n_truncated || max_allocated_blocks < 0) return KV_ERR_ARG;
+  *n_evicted = *n_truncated = 0;
+  const std::vector<int32_t> cand = eviction_candidates(p, alpha, beta, gamma);
+  int32_t n = 0;
+  std::vector<int32_t> kept;
+  KV_TRY(run_release(p, cand, max_allocated_blocks, S(stream), &n, &kept));
+  const int64_t B = p->cfg.block_size;
+  for (int i = 0; i < n; ++i) {
+    StateRec& r = p->slots[cand[2 * i]];
+    const int32_t k = kept[i];
+    if (k < 0 || k > r.nblocks) return KV_ERR_INTERNAL;
+    if (k == r.nblocks) continue;  // only shared blocks: nothing given up
+    p->leave_group(r);             // what remains ends on a whole block
+    if (k == 0) {
+      r.status = ST_EVICTED;
+      ++*n_evicted;
+    } else {
+      r.nblocks = k;
+      r.n = k * B;
+      ++*n_truncated;
+    }
+  }
   return KV_OK;
 }
 

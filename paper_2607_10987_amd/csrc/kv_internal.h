@@ -99,15 +99,26 @@ hipError_t launch_fork(DevHeader* hdr, int32_t* tables, int32_t max_blocks, int3
                        const ForkArgs& a, hipStream_t s);
 hipError_t launch_release(DevHeader* hdr, int32_t* ring, int32_t* rc, const int32_t* tables,
                           int32_t max_blocks, int32_t P, const int32_t* cand, int32_t n_cand,
-                          int64_t max_alloc, int64_t head, int64_t tail, hipStream_t s);
+                          int64_t max_alloc, int64_t head, int64_t tail, int32_t truncate,
+                          int32_t* kept, hipStream_t s);
 hipError_t launch_compose_meta(DevHeader* hdr, int32_t* ring, int32_t* rc, int32_t* tables,
                                int32_t max_blocks, int32_t P, int32_t B, int64_t head,
                                int32_t ncopy, const ComposeArgs& a, hipStream_t s);
 
+// Payload checksum accumulators: pairs (s1, s2) in kSumSlots slots of the
+// metadata area, zero between checksummed copies (k_csum_final clears them).
+constexpr int kSumSlots = 1024;
+
+// slots != null: also add the checksum terms of the bytes copied, the launch's
+// first block starting at payload chunk (16 bytes) index base16.
 hipError_t launch_pack(const PoolGeom& g, int dtype, const int32_t* trow, int64_t b0,
-                       int32_t nblk, int32_t last_valid, void* dst, hipStream_t s);
+                       int32_t nblk, int32_t last_valid, void* dst, unsigned long long* slots,
+                       int64_t base16, hipStream_t s);
 hipError_t launch_unpack(const PoolGeom& g, int dtype, const int32_t* trow, int32_t nblk,
-                         const void* src, hipStream_t s);
+                         const void* src, unsigned long long* slots, int64_t base16,
+                         hipStream_t s);
+// out[0..1] = the slots' sums (s1, s2); clears the slots.
+hipError_t launch_csum_final(unsigned long long* slots, unsigned long long* out, hipStream_t s);
 hipError_t launch_cow(const PoolGeom& g, int dtype, const int2* cow_pairs, const AllocArgs& a,
                       hipStream_t s);
 hipError_t launch_compose_copy(const PoolGeom& g, int dtype, const ComposeArgs& a,

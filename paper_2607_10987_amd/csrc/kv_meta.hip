@@ -94,11 +94,16 @@ __device__ inline int block_scan(int flag, int* excl, int* wave_tot) {
 }
 
 // cand: pairs (slot, n_blocks) in release order.  max_alloc < 0 releases all.
+// truncate != 0: a candidate gives up only the blocks from its first unshared
+// one (refcount 1) on, and kept[c] receives the number of leading blocks it
+// keeps (0: released whole; n_blocks: nothing to give up, untouched).
+// hdr->n_evicted = candidates visited before the budget was met.
 __global__ void __launch_bounds__(kMetaThreads)
 k_release(DevHeader* hdr, int32_t* ring, int32_t* rc, const int32_t* tables,
           int32_t max_blocks, int32_t P, const int32_t* cand, int32_t n_cand,
-          int64_t max_alloc, int64_t head, int64_t tail) {
+          int64_t max_alloc, int64_t head, int64_t tail, int32_t truncate, int32_t* kept) {
   __shared__ int ok;
+  __shared__ int first_own;
   __shared__ int wave_tot[kMetaThreads / 64];
   if (threadIdx.x == 0) ok = hdr->status == 0 && hdr->head == head && hdr->tail == tail;
   __syncthreads();
@@ -109,7 +114,22 @@ k_release(DevHeader* hdr, int32_t* ring, int32_t* rc, const int32_t* tables,
     const int32_t slot = cand[2 * c];
     const int32_t nb = cand[2 * c + 1];
     const int32_t* trow = tables + (int64_t)slot * max_blocks;
-    for (int j0 = 0; j0 < nb; j0 += blockDim.x) {
+    int start = 0;
+    if (truncate) {
+      if (threadIdx.x == 0) first_own = nb;
+      __syncthreads();
+      for (int j = threadIdx.x; j < nb; j += blockDim.x)
+        if (rc[trow[j]] == 1) atomicMin(&first_own, j);
+      __syncthreads();
+      start = first_own;
+      if (threadIdx.x == 0) kept[c] = start;
+      __syncthreads();  // first_own is reset by the next candidate
+      if (start == nb) {
+        ++n_ev;
+        continue;
+      }
+    }
+    for (int j0 = start; j0 < nb; j0 += blockDim.x) {
       const int j = j0 + threadIdx.x;
       int flag = 0;
       int32_t b = -1;
@@ -182,9 +202,10 @@ hipError_t launch_fork(DevHeader* hdr, int32_t* tables, int32_t max_blocks, int3
 
 hipError_t launch_release(DevHeader* hdr, int32_t* ring, int32_t* rc, const int32_t* tables,
                           int32_t max_blocks, int32_t P, const int32_t* cand, int32_t n_cand,
-                          int64_t max_alloc, int64_t head, int64_t tail, hipStream_t s) {
+                          int64_t max_alloc, int64_t head, int64_t tail, int32_t truncate,
+                          int32_t* kept, hipStream_t s) {
   k_release<<<1, kMetaThreads, 0, s>>>(hdr, ring, rc, tables, max_blocks, P, cand, n_cand,
-                                       max_alloc, head, tail);
+                                       max_alloc, head, tail, truncate, kept);
   return hipGetLastError();
 }
 

@@ -54,10 +54,13 @@ __device__ inline PieceIdx piece_idx(int pieces, int L) {
 // Copy piece `piece` of a slab of n16 16-byte chunks; chunk c belongs to
 // slot (c / row16) % B and is replaced by zeros when that slot is >= valid.
 // Loads are non-temporal; stores too unless PLAIN_ST (measured faster for the
-// scattered pool-block writes of unpack).
-template <bool PLAIN_ST = false>
+// scattered pool-block writes of unpack).  With CSUM, the thread also adds
+// the payload checksum terms of the chunks it copied (what it stores) to
+// s1, s2; base16 is the payload chunk index of the slab's chunk 0.
+template <bool PLAIN_ST, bool CSUM>
 __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                  int piece, int n16, int row16, int B, int valid) {
+                                  int piece, int n16, int row16, int B, int valid,
+                                  int64_t base16, uint64_t& s1, uint64_t& s2) {
   const int c0 = piece * (kPiece / 16) + threadIdx.x;
   uint4 v[kUnroll];
 #pragma unroll
@@ -71,15 +74,53 @@ __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restri
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     const int c = c0 + u * kMoveThreads;
-    if (c < n16) { if (PLAIN_ST) dst[c] = v[u]; else st_nt(dst + c, v[u]); }
+    if (c < n16) {
+      if (PLAIN_ST) dst[c] = v[u];
+      else st_nt(dst + c, v[u]);
+      if (CSUM) {
+        // words 4C .. 4C+3 of the payload, weights 4C+1 .. 4C+4
+        const uint64_t w = (uint64_t)v[u].x + v[u].y + v[u].z + v[u].w;
+        const uint64_t C = (uint64_t)(base16 + c);
+        s1 += w;
+        s2 += (4 * C + 1) * w + v[u].y + 2ull * v[u].z + 3ull * v[u].w;
+      }
+    }
+  }
+}
+
+// Workgroup sum of the checksum terms, added to one of kSumSlots slots
+// (spread by workgroup id so that few workgroups meet on one address).
+__device__ inline void csum_commit(uint64_t s1, uint64_t s2, unsigned long long* slots) {
+  __shared__ uint64_t part[2][kMoveThreads / 64];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    s1 += __shfl_xor((unsigned long long)s1, o);
+    s2 += __shfl_xor((unsigned long long)s2, o);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    part[0][wave] = s1;
+    part[1][wave] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t a = 0, b = 0;
+    for (int i = 0; i < kMoveThreads / 64; ++i) {
+      a += part[0][i];
+      b += part[1][i];
+    }
+    unsigned long long* slot = slots + 2 * (blockIdx.x % kSumSlots);
+    atomicAdd(slot, (unsigned long long)a);
+    atomicAdd(slot + 1, (unsigned long long)b);
   }
 }
 
 // grid pieces x L x nblk (flattened): buffer block i, layer l  <-  pool
 // block trow[b0 + i], layer l
+template <bool CSUM>
 __global__ void __launch_bounds__(kMoveThreads)
 k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t nblk,
-       int32_t last_valid, char* dst) {
+       int32_t last_valid, char* dst, int64_t base16, unsigned long long* slots) {
   const PieceIdx pi = piece_idx(pieces, g.L);
   const int i = pi.block, l = pi.layer;
   const int64_t block_bytes = g.block_elems * elt;
@@ -88,14 +129,19 @@ k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t
   const char* s = (const char*)g.pool + id * block_bytes + l * layer_bytes;
   char* d = dst + i * block_bytes + l * layer_bytes;
   const int valid = (i == nblk - 1) ? last_valid : g.B;
-  copy_piece((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16), g.dh * elt / 16, g.B,
-             valid);
+  uint64_t s1 = 0, s2 = 0;
+  copy_piece<false, CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
+                          g.dh * elt / 16, g.B, valid,
+                          base16 + (i * block_bytes + l * layer_bytes) / 16, s1, s2);
+  if (CSUM) csum_commit(s1, s2, slots);
 }
 
 // grid pieces x L x nblk (flattened): pool block trow[i], layer l  <-  buffer
 // block i, layer l
+template <bool CSUM>
 __global__ void __launch_bounds__(kMoveThreads)
-k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src) {
+k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src, int64_t base16,
+         unsigned long long* slots) {
   const PieceIdx pi = piece_idx(pieces, g.L);
   const int i = pi.block, l = pi.layer;
   const int64_t block_bytes = g.block_elems * elt;
@@ -103,8 +149,45 @@ k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src) 
   const int32_t id = trow[i];
   const char* s = src + i * block_bytes + l * layer_bytes;
   char* d = (char*)g.pool + id * block_bytes + l * layer_bytes;
-  copy_piece<true>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
-                   g.dh * elt / 16, g.B, g.B);
+  uint64_t s1 = 0, s2 = 0;
+  copy_piece<true, CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
+                         g.dh * elt / 16, g.B, g.B,
+                         base16 + (i * block_bytes + l * layer_bytes) / 16, s1, s2);
+  if (CSUM) csum_commit(s1, s2, slots);
+}
+
+// One workgroup: out = sum of the slots (mod 2^64), slots cleared for the
+// next checksummed copy.
+__global__ void __launch_bounds__(kMoveThreads)
+k_csum_final(unsigned long long* slots, unsigned long long* out) {
+  __shared__ uint64_t part[2][kMoveThreads / 64];
+  uint64_t s1 = 0, s2 = 0;
+  for (int i = threadIdx.x; i < kSumSlots; i += kMoveThreads) {
+    s1 += slots[2 * i];
+    s2 += slots[2 * i + 1];
+    slots[2 * i] = 0;
+    slots[2 * i + 1] = 0;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    s1 += __shfl_xor((unsigned long long)s1, o);
+    s2 += __shfl_xor((unsigned long long)s2, o);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    part[0][wave] = s1;
+    part[1][wave] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t a = 0, b = 0;
+    for (int i = 0; i < kMoveThreads / 64; ++i) {
+      a += part[0][i];
+      b += part[1][i];
+    }
+    out[0] = a;
+    out[1] = b;
+  }
 }
 
 // grid (n_req, L): for requests with cow > 0, copy slots [0, cow) of every
@@ -357,25 +440,41 @@ k_compose_copy(PoolGeom g, ComposeArgs a, CopyRuns runs) {
 }  // namespace
 
 hipError_t launch_pack(const PoolGeom& g, int dtype, const int32_t* trow, int64_t b0,
-                       int32_t nblk, int32_t last_valid, void* dst, hipStream_t s) {
+                       int32_t nblk, int32_t last_valid, void* dst, unsigned long long* slots,
+                       int64_t base16, hipStream_t s) {
   const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
   const int64_t layer_bytes = g.block_elems * elt / g.L;
   const int pieces = (int)((layer_bytes + kPiece - 1) / kPiece);
   const int64_t n = (int64_t)pieces * g.L * nblk;
   if (n > 0x7fffffff) return hipErrorInvalidValue;
-  k_pack<<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk, last_valid,
-                                              (char*)dst);
+  if (slots)
+    k_pack<true><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk, last_valid,
+                                                      (char*)dst, base16, slots);
+  else
+    k_pack<false><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk,
+                                                       last_valid, (char*)dst, 0, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const PoolGeom& g, int dtype, const int32_t* trow, int32_t nblk,
-                         const void* src, hipStream_t s) {
+                         const void* src, unsigned long long* slots, int64_t base16,
+                         hipStream_t s) {
   const int elt = dtype == KV_DTYPE_BF16 ? 2 : 4;
   const int64_t layer_bytes = g.block_elems * elt / g.L;
   const int pieces = (int)((layer_bytes + kPiece - 1) / kPiece);
   const int64_t n = (int64_t)pieces * g.L * nblk;
   if (n > 0x7fffffff) return hipErrorInvalidValue;
-  k_unpack<<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, (const char*)src);
+  if (slots)
+    k_unpack<true><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, (const char*)src,
+                                                        base16, slots);
+  else
+    k_unpack<false><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow,
+                                                         (const char*)src, 0, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_csum_final(unsigned long long* slots, unsigned long long* out, hipStream_t s) {
+  k_csum_final<<<1, kMoveThreads, 0, s>>>(slots, out);
   return hipGetLastError();
 }
 

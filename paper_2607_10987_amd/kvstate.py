@@ -25,10 +25,13 @@ KV_ERR_BUFSIZE = -6
 KV_ERR_CAPACITY = -7
 KV_ERR_HIP = -8
 KV_ERR_INTERNAL = -9
+KV_ERR_CHECKSUM = -10
+KV_ERR_IO = -11
 KV_DTYPE_F32 = 0
 KV_DTYPE_BF16 = 1
 KV_PACK_MAGIC = 0x5453564B
-KV_PACK_VERSION = 1
+KV_PACK_VERSION = 2
+KV_PACK_CHECKSUM = 1
 KV_MAX_BATCH = 64
 KV_MAX_SEGMENTS = 64
 KV_MAX_FORK = 64
@@ -54,7 +57,9 @@ class kv_pack_header(ctypes.Structure):
                 ("pos_begin", ctypes.c_int64), ("n_tokens", ctypes.c_int64),
                 ("blk_begin", ctypes.c_int64), ("n_blocks", ctypes.c_int64),
                 ("block_bytes", ctypes.c_uint64), ("payload_bytes", ctypes.c_uint64),
-                ("lineage", ctypes.c_uint64), ("src_state_id", ctypes.c_int64)]
+                ("lineage", ctypes.c_uint64), ("src_state_id", ctypes.c_int64),
+                ("flags", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("checksum", ctypes.c_uint64 * 2)]
 
 
 class KVError(RuntimeError):
@@ -84,8 +89,13 @@ _SIGS = {
     "kv_compose": (_I32, [_P, ctypes.POINTER(kv_segment), _I32, _P, _PI64]),
     "kv_pack": (_I32, [_P, _I64, _I64, _I64, _P, _SZ, _PHDR, _P]),
     "kv_unpack": (_I32, [_P, _PHDR, _P, _SZ, _P, _PI64]),
+    "kv_pack_checked": (_I32, [_P, _I64, _I64, _I64, _P, _SZ, _PHDR, _P]),
+    "kv_checkpoint_save": (_I32, [_P, _I64, ctypes.c_char_p, _P]),
+    "kv_checkpoint_load": (_I32, [_P, ctypes.c_char_p, _P, _PI64]),
     "kv_attend": (_I32, [_P, _PI64, _I32, _P, _I64, _P, _P]),
     "kv_evict": (_I32, [_P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double, _P, _PI32]),
+    "kv_evict_truncate": (_I32, [_P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double, _P,
+                                 _PI32, _PI32]),
     "kv_release": (_I32, [_P, _I64, _P]),
     "kv_pin": (_I32, [_P, _I64, _I32]),
     "kv_sync": (_I32, [_P, _P]),
@@ -226,6 +236,28 @@ def kv_pack(pool, state: int, blk_begin: int, blk_end: int, dst, dst_bytes=None,
     return hdr
 
 
+def kv_pack_checked(pool, state: int, blk_begin: int, blk_end: int, dst, dst_bytes=None,
+                    stream=None):
+    hdr = kv_pack_header()
+    if dst_bytes is None:
+        dst_bytes = _nbytes(dst)
+    _check(lib().kv_pack_checked(pool, state, blk_begin, blk_end, _ptr(dst), dst_bytes,
+                                 ctypes.byref(hdr), _stream(stream)), "kv_pack_checked")
+    return hdr
+
+
+def kv_checkpoint_save(pool, state: int, path: str, stream=None):
+    _check(lib().kv_checkpoint_save(pool, state, os.fsencode(path), _stream(stream)),
+           "kv_checkpoint_save")
+
+
+def kv_checkpoint_load(pool, path: str, stream=None) -> int:
+    out = _I64()
+    _check(lib().kv_checkpoint_load(pool, os.fsencode(path), _stream(stream), ctypes.byref(out)),
+           "kv_checkpoint_load")
+    return out.value
+
+
 def kv_unpack(pool, hdr: kv_pack_header, src, src_bytes=None, stream=None) -> int:
     if src_bytes is None:
         src_bytes = _nbytes(src)
@@ -246,6 +278,16 @@ def kv_evict(pool, max_allocated_blocks: int, alpha=0.0, beta=0.0, gamma=1.0, st
     _check(lib().kv_evict(pool, max_allocated_blocks, alpha, beta, gamma, _stream(stream),
                           ctypes.byref(n)), "kv_evict")
     return n.value
+
+
+def kv_evict_truncate(pool, max_allocated_blocks: int, alpha=0.0, beta=0.0, gamma=1.0,
+                      stream=None):
+    """Returns (states evicted whole, states truncated to their shared prefix)."""
+    ne, nt = _I32(), _I32()
+    _check(lib().kv_evict_truncate(pool, max_allocated_blocks, alpha, beta, gamma,
+                                   _stream(stream), ctypes.byref(ne), ctypes.byref(nt)),
+           "kv_evict_truncate")
+    return ne.value, nt.value
 
 
 def kv_release(pool, state: int, stream=None):

@@ -25,7 +25,8 @@ def test_struct_layouts_match_header():
     # kv_model_cfg: 10 int32 + double + uint64
     assert ctypes.sizeof(kv.kv_model_cfg) == 56
     assert ctypes.sizeof(kv.kv_segment) == 24
-    assert ctypes.sizeof(kv.kv_pack_header) == 8 + 8 + 56 + 4 * 8 + 3 * 8 + 8
+    # ... + flags, reserved (2 uint32) + checksum (2 uint64)
+    assert ctypes.sizeof(kv.kv_pack_header) == 8 + 8 + 56 + 4 * 8 + 3 * 8 + 8 + 8 + 16
 
 
 def test_host_only_calls():

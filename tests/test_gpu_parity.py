@@ -53,6 +53,34 @@ def test_allocator_hand_trace_on_device(gpu_available):
     tw.close()
 
 
+def test_evict_truncate_on_device(gpu_available):
+    """Truncation to the shared prefix, then a resume of a truncated state:
+    tables, refcounts, ring and the attention output match the oracle."""
+    tw = Twin(small_shape(), n_blocks=16, max_pos=64, wl="trunc")
+    s0 = tw.materialize(4)
+    c1, c2 = tw.fork(s0, 2)
+    tw.attend([c1], 3)
+    tw.attend([c2], 1)
+    s3 = tw.materialize(3)
+    assert tw.evict_truncate(3) == (1, 2)
+    assert kv.kv_read_block_table(tw.gpu.h, c1) == [0, 1]
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_fork(tw.gpu.h, s3, 1)
+    assert e.value.status == kv.KV_ERR_EVICTED
+    tw.attend([c1, c2], 2)
+    # a shared partial tail: both holders keep only the whole shared blocks
+    r = tw.materialize(5)
+    k, = tw.fork(r, 1)
+    tw.attend([k], 1)
+    kv.kv_pin(tw.gpu.h, c1, 1)
+    tw.orc.pin(tw.sid[c1], True)
+    kv.kv_pin(tw.gpu.h, c2, 1)
+    tw.orc.pin(tw.sid[c2], True)
+    tw.evict_truncate(0)
+    tw.attend([r, k], 1)
+    tw.close()
+
+
 @pytest.mark.parametrize("seed", [1, 2, 3])
 def test_random_sequences_on_device(gpu_available, seed):
     rng = np.random.default_rng(seed)
@@ -62,7 +90,7 @@ def test_random_sequences_on_device(gpu_available, seed):
     handles = []
     for step in range(40):
         live = [h for h in handles if tw.orc.states[tw.sid[h]].status == "ACTIVE"]
-        op = int(rng.integers(0, 7)) if live else 0
+        op = int(rng.integers(0, 8)) if live else 0
         try:
             if op == 0:
                 handles.append(tw.materialize(int(rng.integers(1, 12)),
@@ -89,6 +117,8 @@ def test_random_sequences_on_device(gpu_available, seed):
                 handles.append(tw.unpack(hdr, ohdr, buf, pay, rerotated=h in tw.rerot))
             elif op == 5:
                 tw.evict(int(rng.integers(0, 40)))
+            elif op == 6:
+                tw.evict_truncate(int(rng.integers(0, 40)))
             else:
                 tw.release(live[rng.integers(len(live))])
         except kv.KVError as e:

@@ -113,6 +113,52 @@ def test_eviction_score_general_and_ties():
     assert p.evict(0) == 2 and p.allocated() == 4
 
 
+def test_evict_truncate_hand_trace():
+    p = meta_pool(P=16, B=2)
+    s0, _ = p.materialize(None, T=4)                 # [0, 1], clock 1
+    c1, c2 = p.fork(s0, 2)                           # clock 2 (s0), 3, 4
+    p.attend([c1], T=3)                              # c1 [0, 1, 2, 3], 7 tokens, clock 5
+    p.attend([c2], T=1)                              # c2 [0, 1, 4], 5 tokens, clock 6
+    s3, _ = p.materialize(None, T=3)                 # [5, 6], clock 7
+    assert p.allocated() == 7
+    # LRU order s0, c1, c2, s3.  s0 holds only shared blocks: nothing to give
+    # up, skipped.  c1 keeps [0, 1] (first unshared block at index 2) and frees
+    # 2, 3; c2 frees 4; allocated is then 4 > 3, so s3 (no shared block) goes
+    # whole: 5, 6.
+    assert p.evict_truncate(3) == (1, 2)
+    rc, ring, head, tail = p.allocator()
+    assert list(rc[:8]) == [3, 3, 0, 0, 0, 0, 0, 0]
+    assert (head, tail) == (7, 21) and list(ring[:5]) == [2, 3, 4, 5, 6]
+    assert p.info(c1)[:3] == (0, 4, 2) and p.info(c2)[:3] == (0, 4, 2)
+    assert p.info(s0)[:3] == (0, 4, 2)
+    with pytest.raises(OracleError) as e:
+        p.fork(s3, 1)
+    assert e.value.status == Status.EVICTED
+    # a truncated state resumes as usual: its tail is a whole block
+    p.attend([c1], T=1)
+    assert p.table(c1) == [0, 1, 7]
+    # under budget: nothing happens
+    assert p.evict_truncate(16) == (0, 0)
+
+
+def test_evict_truncate_shared_partial_tail():
+    p = meta_pool(P=16, B=2)
+    s0, _ = p.materialize(None, T=5)                 # [0, 1, 2], block 2 holds 1 token
+    c1, = p.fork(s0, 1)
+    p.attend([c1], T=1)                              # COW: c1 [0, 1, 3]; block 2 now s0's alone
+    assert p.refcount[2] == 1 and p.refcount[3] == 1
+    # order s0 (older), c1: both keep the two shared leading blocks
+    assert p.evict_truncate(2) == (0, 2)
+    assert p.table(s0) == [0, 1] and p.table(c1) == [0, 1]
+    assert p.info(s0)[1] == 4 and p.info(c1)[1] == 4
+    rc, ring, head, tail = p.allocator()
+    assert list(rc[:4]) == [2, 2, 0, 0] and list(ring[:2]) == [2, 3] and tail == 18
+    # pinned states are not candidates
+    p.pin(s0, True)
+    p.pin(c1, True)
+    assert p.evict_truncate(0) == (0, 0)
+
+
 def test_exp4_block_counts_full_size():
     # memory claim of the paper's memory-efficiency experiment as exact counts:
     # a fork grows with the continuation, not with the prefix
@@ -186,7 +232,7 @@ def check_invariants(p: OraclePool):
     assert used | set(free) == set(range(p.P))
 
 
-ops = st.lists(st.tuples(st.integers(0, 6), st.integers(0, 1000), st.integers(0, 1000),
+ops = st.lists(st.tuples(st.integers(0, 7), st.integers(0, 1000), st.integers(0, 1000),
                          st.integers(1, 9)), min_size=1, max_size=25)
 
 
@@ -219,6 +265,8 @@ def test_random_sequences_keep_invariants(seq):
                 p.unpack(hdr)
             elif op == 5:
                 p.evict(a % 25, 0.0, 0.0, 1.0)
+            elif op == 6:
+                p.evict_truncate(a % 25, 0.0, 0.0, 1.0)
             else:
                 p.release(live[a % len(live)])
         except OracleError as e:

@@ -258,6 +258,13 @@ class Twin:
         self._after()
         return n
 
+    def evict_truncate(self, max_alloc: int, a=0.0, b=0.0, g=1.0):
+        r = kv.kv_evict_truncate(self.gpu.h, max_alloc, a, b, g)
+        ro = self.orc.evict_truncate(max_alloc, a, b, g)
+        assert r == ro
+        self._after()
+        return r
+
     def release(self, h):
         kv.kv_release(self.gpu.h, h)
         self.orc.release(self.sid[h])
