@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--transfer-sweep", action="store_true",
                     help="instead of the step: measured materialize vs pack + unpack per context "
                          "length, and the transfer-vs-recompute decision at several link rates")
+    ap.add_argument("--checkpoint-sweep", action="store_true",
+                    help="instead of the step: plain vs checksummed pack / unpack and file "
+                         "checkpoint save / load per context length")
     return ap.parse_args()
 
 
@@ -232,6 +235,100 @@ def transfer_sweep(args, kv, torch, synth):
     print(json.dumps({"experiment": "transfer vs recompute (8B shape, one MI355X)",
                       "data": "synthetic", "rows": rows}), flush=True)
 
+def checkpoint_sweep(args, kv, torch, synth):
+    """Cost of integrity and persistence on the 8B shape: the pack / unpack
+    kernels with and without the fused payload checksum (kernel time from the
+    library's events, and the whole call including the checksum read-back),
+    and file checkpoints (save / load through pinned staging, wall time)."""
+    import tempfile
+    wl = synth.WORKLOADS["fork4-8b"]
+    s = wl.shape
+    dev = "cuda"
+    tdt = torch.bfloat16
+    L, d, cols, B = s.n_layers, s.d_model, s.qkv_cols, s.block_size
+    lengths = [1024, 4096, 16384]
+    nmax = lengths[-1]
+    cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, nmax + 64, 8,
+                      s.rope_base, 1)
+    n_blocks = 2 * (nmax // B) + 64
+    pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, nmax, 1, nmax + 64))
+    w = torch.empty((L, cols, d), dtype=tdt, device=dev)
+    for layer in range(L):
+        w[layer] = synth.normal_torch(synth.w_key(args.seed, wl.name, layer), (cols, d), s.w_std,
+                                      s.dtype, dev)
+    pool.set_weights(w, cols * d)
+    x = synth.normal_torch(synth.x_key(args.seed, wl.name, 0), (nmax, d), 1.0, s.dtype, dev)
+    o = torch.empty((L, nmax, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
+    buf = torch.empty((nmax // B) * s.block_bytes, dtype=torch.uint8, device=dev)
+    tmpdir = tempfile.mkdtemp(prefix="kvck")
+    path = os.path.join(tmpdir, "state.kvck")
+    rows = []
+
+    def wall(fn):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = fn()
+        torch.cuda.synchronize()
+        return r, time.perf_counter() - t0
+
+    for n in lengths:
+        st = kv.kv_materialize(pool.h, x[:n], n, 0, o[:, :n])
+        nb = kv.kv_state_info(pool.h, st)["n_blocks"]
+        kvb = nb * s.block_bytes
+        t = {k: [] for k in ("pack_k", "packc_k", "unpack_k", "unpackc_k", "packc_w",
+                             "unpackc_w", "save_w", "load_w")}
+        for rep in range(4):
+            kv.kv_profile_enable(pool.h, True)
+            kv.kv_profile_read(pool.h)
+            hdr = kv.kv_pack(pool.h, st, 0, nb, buf)
+            u = kv.kv_unpack(pool.h, hdr, buf)
+            p0 = kv.kv_profile_read(pool.h)
+            kv.kv_release(pool.h, u)
+            kv.kv_profile_read(pool.h)
+            hc, tw = wall(lambda: kv.kv_pack_checked(pool.h, st, 0, nb, buf))
+            uc, tu = wall(lambda: kv.kv_unpack(pool.h, hc, buf))
+            p1 = kv.kv_profile_read(pool.h)
+            kv.kv_profile_enable(pool.h, False)
+            kv.kv_release(pool.h, uc)
+            _, ts = wall(lambda: kv.kv_checkpoint_save(pool.h, st, path))
+            v, tl = wall(lambda: kv.kv_checkpoint_load(pool.h, path))
+            kv.kv_release(pool.h, v)
+            os.remove(path)
+            if rep == 0:
+                continue  # warm-up
+            t["pack_k"].append(p0["pack"][1])
+            t["unpack_k"].append(p0["unpack"][1])
+            t["packc_k"].append(p1["pack"][1])
+            t["unpackc_k"].append(p1["unpack"][1])
+            t["packc_w"].append(tw * 1e3)
+            t["unpackc_w"].append(tu * 1e3)
+            t["save_w"].append(ts * 1e3)
+            t["load_w"].append(tl * 1e3)
+        kv.kv_release(pool.h, st)
+        m = {k: min(v) for k, v in t.items()}
+
+        def gbs(ms):
+            return round(2 * kvb / (ms * 1e-3) / 1e9, 1)  # read + write bytes
+
+        rows.append({
+            "tokens": n, "kv_bytes": kvb,
+            "pack": {"ms": round(m["pack_k"], 4), "GBs": gbs(m["pack_k"])},
+            "pack_checked": {"kernel_ms": round(m["packc_k"], 4), "GBs": gbs(m["packc_k"]),
+                             "call_ms": round(m["packc_w"], 4)},
+            "unpack": {"ms": round(m["unpack_k"], 4), "GBs": gbs(m["unpack_k"])},
+            "unpack_checked": {"kernel_ms": round(m["unpackc_k"], 4), "GBs": gbs(m["unpackc_k"]),
+                               "call_ms": round(m["unpackc_w"], 4)},
+            "checkpoint": {"save_ms": round(m["save_w"], 2), "load_ms": round(m["load_w"], 2),
+                           "save_GBs": round(kvb / (m["save_w"] * 1e-3) / 1e9, 2),
+                           "load_GBs": round(kvb / (m["load_w"] * 1e-3) / 1e9, 2)}})
+        print(f"[bench] checkpoint sweep {n} tokens done", file=sys.stderr, flush=True)
+    os.rmdir(tmpdir)
+    pool.close()
+    print(json.dumps({"experiment": "checksum and checkpoint cost (8B shape, one MI355X)",
+                      "rate_bytes": "pack / unpack GB/s count read + write bytes; checkpoint "
+                                    "GB/s count the payload once",
+                      "data": "synthetic", "rows": rows}), flush=True)
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -248,6 +345,9 @@ def main():
         sys.exit(2)
     if args.transfer_sweep:
         transfer_sweep(args, kv, torch, synth)
+        return
+    if args.checkpoint_sweep:
+        checkpoint_sweep(args, kv, torch, synth)
         return
     wl = synth.WORKLOADS[args.workload]
     s = wl.shape
