@@ -31,7 +31,12 @@
 // Software pipeline: iteration t issues the QK^T products of tile t + 1
 // before the softmax of tile t, so that the matrix cores can work on the next
 // scores while the vector ALUs exponentiate the current ones; then the PV
-// products of tile t.
+// products of tile t.  The loop is peeled so that its body has no branch
+// between those products and the softmax (the only branch left is the rare
+// accumulator rescale, placed after the exponentials): the last tile is
+// handled after the loop, and the tiles that no query of the wave masks run
+// in a loop of their own without mask code (the mask is applied only on the
+// causal diagonal and on ragged ends).
 //
 // Workgroup order: consecutive workgroups are dispatched round-robin to the
 // 8 XCDs, each with its own L2.  The linear workgroup id is permuted so that
@@ -40,6 +45,7 @@
 // one L2.
 #include "kv_dma.h"
 #include "kv_fast.h"
+#include <type_traits>
 
 namespace kvs {
 
@@ -207,8 +213,6 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   float m_run = -INFINITY, l_run = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // Copies of one wave complete in order, 4 per tile: a tile is ready once at
-  // most the 4 k copies of the k tiles issued after it are pending.
   static_assert(kPS >= 3 && kPS <= 4, "stages");
   auto wait_tiles = [](int k) {
     if (k >= 2)
@@ -218,50 +222,33 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     else
       wait_vmcnt<0>();
   };
-  for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
-  wait_tiles(min(kPS - 1, n_tiles) - 1);
-  lds_barrier();
-  floatx16 sacc[2];
-  qk(0, sacc);
 
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const bool has_next = tile + 1 < n_tiles;
-    floatx16 snext[2];
-    if (has_next) {
-      // tile + 1 ready, and every wave is done with tile - 1, whose buffer
-      // is refilled
-      wait_tiles(min(tile + kPS - 1, n_tiles) - (tile + 2));
-      lds_barrier();
-      if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
-      qk((tile + 1) % kPS, snext);
-    }
-    const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
+  // softmax of one tile's scores: mask (MASKED only), running max, exp2,
+  // bf16 probabilities pf and their row sum; returns whether the max moved
+  float ps = 0.f, m_new = 0.f, m_use = 0.f;
+  bf16x8 pf[4];
+  auto softmax = [&](floatx16* sc, int tile, auto masked_c) -> bool {
+    constexpr bool MASKED = decltype(masked_c)::value;
     const int k0 = tile * kKT;
-
-    // wave-uniform: does any (query, key) pair of this tile need masking?
-    const bool need_mask = __builtin_amdgcn_readfirstlane(
-                               (int)(k0 + kKT - 1 > sd.n_before + t0 + tg * 32 ||
-                                     k0 + kKT > n_keys || t0 + tg * 32 + 31 >= a.T)) != 0;
-    if (need_mask) {
+    if constexpr (MASKED) {
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
-          if (kk > uq || kk >= n_keys) sacc[kt][e] = -INFINITY;
+          if (kk > uq || kk >= n_keys) sc[kt][e] = -INFINITY;
         }
     }
     float mt_max = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sacc[kt][e]);
+      for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sc[kt][e]);
     mt_max = max_xor32(mt_max) * qk_scale_log2;
-    const float m_new = mt_max > m_run + 8.f ? mt_max : m_run;
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    m_new = mt_max > m_run + 8.f ? mt_max : m_run;
+    m_use = m_new == -INFINITY ? 0.f : m_new;
     const bool moved = __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run) != 0)) != 0;
     float ps0 = 0.f, ps1 = 0.f;
-    bf16x8 pf[4];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -269,16 +256,24 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         float p[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          p[j] = __builtin_amdgcn_exp2f(fmaf(sacc[kt][hs * 8 + j], qk_scale_log2, -m_use));
+          p[j] = __builtin_amdgcn_exp2f(fmaf(sc[kt][hs * 8 + j], qk_scale_log2, -m_use));
         const uint32_t wv[4] = {cvt2(p[0], p[1]), cvt2(p[2], p[3]), cvt2(p[4], p[5]),
                                 cvt2(p[6], p[7])};
-        // row sum of the bf16 probabilities the PV product uses
         ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[0]), ones, ps0, false);
         ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[1]), ones, ps1, false);
         ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[2]), ones, ps0, false);
         ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[3]), ones, ps1, false);
         pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(const uint4*)wv);
       }
+    ps = ps0 + ps1;
+    // pin the probabilities before the caller's rescale branch, so that the
+    // exponentials stay in the straight-line region with the QK^T products
+#pragma unroll
+    for (int i = 0; i < 4; ++i) settle(pf[i]);
+    settle(ps);
+    return moved;
+  };
+  auto finish = [&](bool moved) {
     if (moved) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
       l_run *= alpha;
@@ -287,9 +282,12 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
     }
-    l_run += ps0 + ps1;
+    l_run += ps;
     m_run = m_new;
-    // O^T += V^T P^T, V^T operands by transposed LDS reads
+  };
+  // O^T += V^T P^T for one tile, V^T operands by transposed LDS reads
+  auto pv = [&](int tile) {
+    const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
     const int gi = lane >> 4, li = lane & 15;
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
@@ -308,11 +306,37 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                                                            oacc[mt], 0, 0, 0);
       }
     }
-    if (has_next) {
-      sacc[0] = snext[0];
-      sacc[1] = snext[1];
-    }
-  }
+  };
+
+  for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
+  wait_tiles(min(kPS - 1, n_tiles) - 1);
+  lds_barrier();
+  floatx16 sacc[2];
+  qk(0, sacc);
+
+  // One step: QK^T of tile + 1 and the softmax of tile in one straight-line
+  // region (interleaved), then the PV product of tile.
+  auto step = [&](int tile, auto masked_c) {
+    wait_tiles(min(tile + kPS - 1, n_tiles) - (tile + 2));
+    lds_barrier();
+    if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
+    floatx16 snext[2];
+    qk((tile + 1) % kPS, snext);
+    const bool moved = softmax(sacc, tile, masked_c);
+    finish(moved);
+    pv(tile);
+    sacc[0] = snext[0];
+    sacc[1] = snext[1];
+  };
+  // tiles whose keys all precede this wave's first query need no mask
+  const int first_q = sd.n_before + t0 + tg * 32;
+  const int n_free = (t0 + tg * 32 + 31 < a.T) ? min((first_q + 1) / kKT, n_keys / kKT) : 0;
+  const int lim = n_tiles - 1;
+  int tile = 0;
+  for (; tile < min(n_free, lim); ++tile) step(tile, std::false_type{});
+  for (; tile < lim; ++tile) step(tile, std::true_type{});
+  finish(softmax(sacc, tile, std::true_type{}));
+  pv(tile);
 
   const float l_tot = sum_xor32(l_run);
   if (!q_valid) return;

@@ -10,13 +10,15 @@
 // i + 64 of the same head) sit in the same lane when one wavefront owns a
 // whole 128-channel head, and stores are 8-byte runs of one token row.
 //
-// Two tilings:
-//   prefill  (T > 1): 256 channels (2 heads) x 256 tokens per workgroup, four
-//            waves of 128 x 128, K step 64, double-buffered LDS (144 KiB),
-//            RoPE in registers, bf16 tile restaged through LDS so that the
-//            final Q / K / V stores are 16-byte, row-contiguous writes;
-//   decode   (T = 1, at most 32 tokens): 128 channels (1 head) x 32 tokens,
-//            four waves of 32 channels, fp32 tile in LDS for the rotation.
+// Kernels, by token count M of the call:
+//   M > 32   k_qkv_dl: 256 channels (2 heads) x 256 tokens per workgroup,
+//            eight waves of 128 x 64, direct global->LDS copies, RoPE in
+//            registers, bf16 tile restaged through LDS so that the final
+//            Q / K / V stores are 16-byte, row-contiguous writes (k_qkv_mfma
+//            with register-staged LDS tiles when d is not a multiple of 64);
+//   M <= 16  k_qkv_decode_lds: weight streaming, token rows staged in LDS;
+//   M <= 32  k_qkv_decode / k_qkv_mfma<128, 32>: 128 channels (1 head) x 32
+//            tokens, fp32 tile in LDS for the rotation.
 // Q goes to the scratch buffer [lc][M][Hq * dh]; K and V rows go to
 // pool[table[slot][u / B]][l][K|V][kv head][u % B][:] with u = n_before + t.
 #include "kv_dma.h"
@@ -264,16 +266,23 @@ k_qkv_mfma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restric
 // Prefill projection, main loop with direct global->LDS loads
 // (global_load_lds_dwordx4: lane i of a wavefront writes LDS bytes
 // [16 i, 16 i + 16) of the instruction's 1 KiB destination) and a 2-stage
-// pipeline of K-steps of 64: one step is in flight while the other is
-// consumed, with no register staging.  Tile 256 channels x 256 tokens, 8
-// wavefronts of 128 channels x 64 tokens (a wave owns a whole head, so RoPE
-// stays in registers).  LDS rows are 128 bytes (64 k); the 16-byte chunk q of
-// row r is stored at chunk slot q ^ f(r), f(r) = (r >> 1) & 7, so that the 16
-// consecutive rows an operand read serves in one LDS cycle (16 lanes x 16
-// bytes over 64 banks) cover the 16 bank groups.
+// pipeline of K-steps of 64, with no register staging.  Tile 256 channels x
+// 256 tokens, 8 wavefronts of 128 channels x 64 tokens (a wave owns a whole
+// head, so RoPE stays in registers).  LDS rows are 128 bytes (64 k); the
+// 16-byte chunk q of row r is stored at chunk slot q ^ f(r), f(r) =
+// (r >> 1) & 7, so that the 16 consecutive rows an operand read serves in one
+// LDS cycle (16 lanes x 16 bytes over 64 banks) cover the 16 bank groups.
+//
+// Operands are read one k-substep (16) ahead of the products that use them,
+// and the one workgroup barrier per K-step sits between the reads and the
+// products of the step's last k-substep: a wave reaches it with those
+// operands already in registers, so its products keep the matrix core busy
+// while the first operands of the next stage are read.  That barrier also
+// frees the stage just consumed, which then receives the copies of the
+// K-step after next.  Copies take a wave-uniform base (scalar registers) and
+// a per-lane 32-bit offset.
 __device__ inline int swz(int r) { return (r >> 1) & 7; }
 
-constexpr int kDlStages = 2;
 constexpr int kDlBK = 64;
 constexpr int kDlWaves = 8;
 constexpr int kDlThreads = 64 * kDlWaves;
@@ -282,40 +291,45 @@ __global__ void __launch_bounds__(kDlThreads, 1)
 k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
          int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0) {
   constexpr int CH = 256, BT = 256;
-  constexpr int OP = CH * kDlBK;                 // elements per operand per stage
+  constexpr int OP = CH * kDlBK;
   constexpr int STAGE = 2 * OP;
-  constexpr int SLD = CH + 8;                    // epilogue row stride
-  constexpr int MAIN = kDlStages * STAGE * 2;
+  constexpr int SLD = CH + 8;
+  constexpr int MAIN = 2 * STAGE * 2;
   constexpr int EPI = BT * SLD * 2;
-  constexpr int LPW = (OP / 8) / 64 / kDlWaves;  // 1 KiB load instructions per wave per operand
+  constexpr int LPW = (OP / 8) / 64 / kDlWaves;  // copies per wave per operand
   constexpr int TI = 4, TJ = 2;
+  constexpr int KS = kDlBK / 16;
   __shared__ __attribute__((aligned(16))) char smem_raw[MAIN > EPI ? MAIN : EPI];
   uint16_t* smem = (uint16_t*)smem_raw;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, hl = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * CH;
   const int m0 = blockIdx.y * BT;
   const int lc = blockIdx.z, l = l0 + lc;
   const int M = a.batch * a.T, d = g.d;
   const uint16_t* wl = w + (int64_t)l * w_stride;
-  const int ch0 = (wave & 1) * 128;        // this wave's head within the tile
-  const int tk0 = (wave >> 1) * (TJ * 32); // this wave's 64 tokens
+  const int ch0 = (wave & 1) * 128;
+  const int tk0 = (wave >> 1) * (TJ * 32);
 
-  const uint16_t* ga[LPW];
-  const uint16_t* gb[LPW];
+  const uint32_t lds0 = lds_addr(smem);
+  uint32_t va[LPW], vb[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     const int c = (wave * LPW + j) * 64 + lane, r = c >> 3, q = (c & 7) ^ swz(r);
-    ga[j] = wl + (int64_t)(n0 + r) * d + q * 8;
-    gb[j] = x + (int64_t)min(m0 + r, M - 1) * d + q * 8;  // rows past M: any valid row
+    va[j] = ((uint32_t)r * d + q * 8) * 2;
+    vb[j] = ((uint32_t)min(r, M - 1 - m0) * d + q * 8) * 2;
   }
+  const char* abase = (const char*)(wl + (int64_t)n0 * d);
+  const char* bbase = (const char*)(x + (int64_t)m0 * d);
   auto issue = [&](int kb, int buf) {
-    uint16_t* As = smem + buf * STAGE;
-    uint16_t* Bs = As + OP;
+    const uint32_t la = lds0 + buf * STAGE * 2 + wave * LPW * 1024;
+    const char* sa = abase + kb * kDlBK * 2;
+    const char* sb = bbase + kb * kDlBK * 2;
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
-      lds_dma16(ga[j] + kb * kDlBK, As + (wave * LPW + j) * 512);
-      lds_dma16(gb[j] + kb * kDlBK, Bs + (wave * LPW + j) * 512);
+      lds_dma16_sv(sa, va[j], la + j * 1024);
+      lds_dma16_sv(sb, vb[j], la + OP * 2 + j * 1024);
     }
   };
 
@@ -327,50 +341,57 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int nk = d / kDlBK;
-  for (int st = 0; st < kDlStages - 1 && st < nk; ++st) issue(st, st);
-  for (int kb = 0; kb < nk; ++kb) {
-    // this wave's loads of stage kb are done when at most the two later
-    // stages (2 x 2 LPW instructions) are outstanding; the barrier extends
-    // that to every wave's share of the stage
-    if (kb + kDlStages - 2 < nk)
-      wait_vmcnt<(kDlStages - 2) * 2 * LPW>();
-    else
-      wait_vmcnt<0>();
-    lds_barrier();
-    if (kb + kDlStages - 1 < nk) issue(kb + kDlStages - 1, (kb + kDlStages - 1) % kDlStages);
-    const uint16_t* As = smem + (kb % kDlStages) * STAGE;
+  bf16x8 fa[2][TI], fb[2][TJ];
+  auto load = [&](int buf, int ks, int sl) {
+    const uint16_t* As = smem + buf * STAGE;
     const uint16_t* Bs = As + OP;
-    // all operands of the stage first, so that only the first products wait
-    // for LDS
-    constexpr int KS = kDlBK / 16;
-    bf16x8 fa[KS][TI], fb[KS][TJ];
+    const int q = ks * 2 + hl;
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const int m = ch0 + i * 32 + (lane & 31);
+      fa[sl][i] = *(const bf16x8*)(As + (m * 8 + (q ^ swz(m))) * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int t = tk0 + j * 32 + (lane & 31);
+      fb[sl][j] = *(const bf16x8*)(Bs + (t * 8 + (q ^ swz(t))) * 8);
+    }
+  };
+
+  const int nk = d / kDlBK;
+  issue(0, 0);
+  if (nk > 1) {
+    issue(1, 1);
+    wait_vmcnt<2 * LPW>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  lds_barrier();
+  load(0, 0, 0);
+  for (int kb = 0; kb < nk; ++kb) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const int q = ks * 2 + hl;
-#pragma unroll
-      for (int i = 0; i < TI; ++i) {
-        const int m = ch0 + i * 32 + (lane & 31);
-        fa[ks][i] = *(const bf16x8*)(As + (m * 8 + (q ^ swz(m))) * 8);
+      if (ks + 1 < KS) {
+        load(kb & 1, ks + 1, (ks + 1) & 1);
+      } else if (kb + 1 < nk) {
+        // stage kb + 1 landed (this wave's copies, then every wave's), and
+        // every wave holds its last operands of stage kb in registers, so
+        // its buffer takes stage kb + 2
+        wait_vmcnt<0>();
+        lds_barrier();
+        load((kb + 1) & 1, 0, 0);
+        if (kb + 2 < nk) issue(kb + 2, kb & 1);
       }
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int t = tk0 + j * 32 + (lane & 31);
-        fb[ks][j] = *(const bf16x8*)(Bs + (t * 8 + (q ^ swz(t))) * 8);
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks & 1][i], fb[ks & 1][j],
+                                                              acc[i][j], 0, 0, 0);
+    }
   }
-  __syncthreads();  // LDS stages become the epilogue's staging tile
+  __syncthreads();
 
-  // ---- epilogue: rotate in registers, restage bf16 rows, 16-byte stores
   const int half = kDh / 2;
   uint16_t* S = smem;
   const int hh = (n0 + ch0) / kDh;
