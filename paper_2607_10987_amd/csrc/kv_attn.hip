@@ -31,12 +31,16 @@
 // Software pipeline: iteration t issues the QK^T products of tile t + 1
 // before the softmax of tile t, so that the matrix cores can work on the next
 // scores while the vector ALUs exponentiate the current ones; then the PV
-// products of tile t.  The loop is peeled so that its body has no branch
-// between those products and the softmax (the only branch left is the rare
-// accumulator rescale, placed after the exponentials): the last tile is
-// handled after the loop, and the tiles that no query of the wave masks run
-// in a loop of their own without mask code (the mask is applied only on the
-// causal diagonal and on ragged ends).
+// products of tile t, in two halves.  The loop is peeled so that its body has
+// no branch between those products and the softmax (the only branch left is
+// the rare accumulator rescale, placed after the exponentials): the last tile
+// is handled after the loop, and the tiles that no query of the wave masks
+// run in a loop of their own without mask code (the mask is applied only on
+// the causal diagonal and on ragged ends).  The one workgroup barrier per
+// tile sits between the two PV halves, so a wave meets it with products
+// still to issue; it makes tile t + 2 visible and frees the buffer of tile
+// t - 1 for the copies of tile t + 3.  The block ids of a tile's copies are
+// read from LDS one issue ahead.
 //
 // Workgroup order: consecutive workgroups are dispatched round-robin to the
 // 8 XCDs, each with its own L2.  The linear workgroup id is permuted so that
@@ -158,6 +162,14 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const int64_t koff = tile_off(g, l, 0, gk, 0), voff = tile_off(g, l, 1, gk, 0);
   const int64_t kv_gap = (voff - koff) * 2;
   const uint32_t lds0 = lds_addr(smem);
+  // block ids of the next full tile's copies, read one issue ahead
+  int nid[2];
+  auto fetch_ids = [&](int tile) {
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+      nid[jj] = s_tbl[min((tile * kKT + (wave + jj * kPW) * 4) >> g.b_shift, nbl - 1)];
+  };
+  fetch_ids(0);
   auto issue = [&](int tile, int buf) {
     if ((tile + 1) * kKT <= key_end) {
       const uint32_t kl = lds0 + buf * 2 * kPTile * 2, vl = kl + kPTile * 2;
@@ -165,7 +177,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int jj = 0; jj < 2; ++jj) {
         const int j = wave + jj * kPW;
         const int key0 = tile * kKT + j * 4;
-        const int id = __builtin_amdgcn_readfirstlane(s_tbl[key0 >> g.b_shift]);
+        const int id = __builtin_amdgcn_readfirstlane(nid[jj]);
         const char* kb = (const char*)pool +
                          ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
         const int r = j * 4 + (lane >> 4);
@@ -188,6 +200,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         lds_dma16(pool + base + voff + ((lane & 15) ^ vswz(r)) * 8, Vs + j * 512);
       }
     }
+    fetch_ids(tile + 1);
   };
   // S^T of one tile for this wave's 32 tokens
   auto qk = [&](int buf, floatx16* sacc) {
@@ -285,12 +298,13 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     l_run += ps;
     m_run = m_new;
   };
-  // O^T += V^T P^T for one tile, V^T operands by transposed LDS reads
-  auto pv = [&](int tile) {
+  // O^T += V^T P^T for keys [16 s_lo, 16 s_hi) of one tile, V^T operands by
+  // transposed LDS reads
+  auto pv = [&](int tile, int s_lo, int s_hi) {
     const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
     const int gi = lane >> 4, li = lane & 15;
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
+    for (int s4 = s_lo; s4 < s_hi; ++s4) {
       const int key_a = s4 * 16 + (gi >> 1) * 4 + (li >> 2);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
@@ -308,27 +322,34 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     }
   };
 
+  // Tiles 0 .. kPS - 2 in flight; tiles 0 and 1 visible before the loop.
   for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
-  wait_tiles(min(kPS - 1, n_tiles) - 1);
+  wait_tiles(min(kPS - 1, n_tiles) - min(2, n_tiles));
   lds_barrier();
   floatx16 sacc[2];
   qk(0, sacc);
 
-  // One step: QK^T of tile + 1 and the softmax of tile in one straight-line
-  // region (interleaved), then the PV product of tile.
+  // One step: QK^T of tile + 1 with the softmax of tile, then the PV product
+  // of tile in two halves with the barrier between them: it makes tile + 2
+  // visible for the next step and frees the buffer of tile - 1.
   auto step = [&](int tile, auto masked_c) {
-    wait_tiles(min(tile + kPS - 1, n_tiles) - (tile + 2));
-    lds_barrier();
-    if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
     floatx16 snext[2];
     qk((tile + 1) % kPS, snext);
     const bool moved = softmax(sacc, tile, masked_c);
     finish(moved);
-    pv(tile);
+    pv(tile, 0, 2);
+    if (tile + 2 < n_tiles) {
+      // copies of one wave complete in order, 4 per tile: tile + 2 is the
+      // newest issued.  Every read of the buffer about to be refilled (tile
+      // - 1) fed a product issued earlier, so no LDS wait is needed here.
+      wait_vmcnt<0>();
+      barrier_only();
+      if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
+    }
+    pv(tile, 2, 4);
     sacc[0] = snext[0];
     sacc[1] = snext[1];
   };
-  // tiles whose keys all precede this wave's first query need no mask
   const int first_q = sd.n_before + t0 + tg * 32;
   const int n_free = (t0 + tg * 32 + 31 < a.T) ? min((first_q + 1) / kKT, n_keys / kKT) : 0;
   const int lim = n_tiles - 1;
@@ -336,7 +357,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   for (; tile < min(n_free, lim); ++tile) step(tile, std::false_type{});
   for (; tile < lim; ++tile) step(tile, std::true_type{});
   finish(softmax(sacc, tile, std::true_type{}));
-  pv(tile);
+  pv(tile, 0, 4);
 
   const float l_tot = sum_xor32(l_run);
   if (!q_valid) return;

@@ -64,6 +64,10 @@ __device__ inline void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Workgroup barrier alone, for a point where the wave's own LDS reads of
+// the buffer other waves are about to refill have already been consumed.
+__device__ inline void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
 template <typename T>
 __device__ inline void settle(T& v) {
   asm volatile("" : "+v"(v));
