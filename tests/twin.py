@@ -131,9 +131,11 @@ class Twin:
         table = kv.kv_read_block_table(self.gpu.h, h)
         n = kv.kv_state_info(self.gpu.h, h)["n_tokens"]
         blocks = self.gpu.blocks_view()[table, layer]         # [nb, 2, Hkv, B, dh]
-        x = to_np(blocks)
-        nb, _, hkv, B, dh = x.shape
-        x = x.transpose(1, 2, 0, 3, 4).reshape(2, hkv, nb * B, dh)[:, :, :n]
+        nb, _, hkv, B, dh = blocks.shape
+        # valid slots only: the slots past the last token are unspecified and
+        # may hold any bit pattern (signalling NaNs included)
+        x = blocks.permute(1, 2, 0, 3, 4).reshape(2, hkv, nb * B, dh)[:, :, :n]
+        x = to_np(x)
         return x[0], x[1]
 
     def check_state_kv(self, h):
