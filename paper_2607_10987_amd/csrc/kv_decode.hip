@@ -474,14 +474,15 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
   const int slots = std::min(nch * a.batch, 2 * nch + a.batch);
   dim3 grid(slots, g.Hkv, lc);
-  // three 16 KiB stages per wave (two in flight): 3-4% faster than two at
-  // 5 waves per CU, while four (2 waves per CU) are 9% slower; the number of
-  // bytes in flight per CU, bounded by LDS, is what limits this stream
+  // one query tile: three 16 KiB stages per wave (two in flight), 3-4%
+  // faster than two, while four are 9% slower; the number of bytes in flight
+  // per CU, bounded by LDS, is what limits this stream.  Two query tiles (more
+  // than 32 query vectors per unit): two stages, 15% faster than three.
   if (a.batch * G <= 32)
     k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, l0, sc);
   else
-    k_decode_stream<2, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+    k_decode_stream<2, 2><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, l0, sc);
   return hipGetLastError();
 }

@@ -277,12 +277,16 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ inline void st_nt16(uint16_t* p, const uint4& v) { st_nt((uint4*)p, v); }
 typedef float floatx2_t __attribute__((ext_vector_type(2)));
 
+constexpr int kComposePieces = 2;
+
 __device__ inline uint32_t cvt_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t){a, b}, bf16x2_t));
 }
 
-// bf16 compose copy.  grid L x copied blocks (flattened, layer fastest), one
-// workgroup per (block, layer) slab.  Work items are 16-byte chunks of key / value rows, a row's
+// bf16 compose copy.  grid kComposePieces x L x copied blocks (flattened,
+// piece fastest): each (block, layer) slab is split over kComposePieces
+// workgroups by KV head (two measured 3% faster than one, four and eight
+// slower).  Work items are 16-byte chunks of key / value rows, a row's
 // chunks on consecutive lanes (1 KiB per wavefront access).  Destination
 // token u = b * B + r comes from segment i (source token u - off_i); keys of
 // a shifted segment are rotated by its shift delta: for frequency index j the
@@ -292,9 +296,10 @@ __device__ inline uint32_t cvt_bf16x2(float a, float b) {
 // shuffle.  All loads of a thread are issued before its stores.
 __global__ void __launch_bounds__(kMoveThreads)
 k_compose_bf16(PoolGeom g, ComposeArgs a, CopyRuns runs) {
-  constexpr int U = 8;  // items per thread per operand and pass
+  constexpr int U = 4;  // items per thread per operand and pass
   __shared__ int32_t s_src[64], s_slot[64], s_delta[64];
-  const int b = copy_run_block(runs, blockIdx.x / g.L), l = blockIdx.x % g.L;
+  const int piece = blockIdx.x % kComposePieces, slab = blockIdx.x / kComposePieces;
+  const int b = copy_run_block(runs, slab / g.L), l = slab % g.L;
   const int tid = threadIdx.x;
   compose_rows(g, a, b, s_src, s_slot, s_delta);
   const int32_t dst = g.tables[(int64_t)a.new_slot * g.max_blocks + b];
@@ -302,8 +307,13 @@ k_compose_bf16(PoolGeom g, ComposeArgs a, CopyRuns runs) {
   uint16_t* pool = (uint16_t*)g.pool;
   uint16_t* dblk = pool + (int64_t)dst * g.block_elems;
   const int cpr = g.dh / 8, hc = cpr / 2, half = g.dh / 2;  // chunks per row, per half row
-  const int n_items = g.Hkv * g.B * cpr;                    // per operand
-  for (int base = 0; base < n_items; base += kMoveThreads * U) {
+  // this workgroup's items (16-byte chunks per operand), whole rows of
+  // whole waves so that a row's chunks stay on consecutive lanes
+  const int n_all = g.Hkv * g.B * cpr;
+  const int per = ((n_all + kComposePieces - 1) / kComposePieces + kMoveThreads - 1) /
+                  kMoveThreads * kMoveThreads;
+  const int i0 = piece * per, n_items = min(n_all, i0 + per);
+  for (int base = i0; base < n_items; base += kMoveThreads * U) {
     uint4 kx[U], vx[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -511,7 +521,8 @@ hipError_t launch_compose_copy(const PoolGeom& g, int dtype, const ComposeArgs& 
   if (total == 0) return hipSuccess;
   dim3 grid(total, g.L);
   if (dtype == KV_DTYPE_BF16 && g.dh >= 16 && (g.dh & (g.dh - 1)) == 0)
-    k_compose_bf16<<<(unsigned)((int64_t)total * g.L), kMoveThreads, 0, s>>>(g, a, runs);
+    k_compose_bf16<<<(unsigned)((int64_t)total * g.L * kComposePieces), kMoveThreads, 0, s>>>(
+        g, a, runs);
   else if (dtype == KV_DTYPE_BF16)
     k_compose_copy<uint16_t><<<grid, kMoveThreads, 0, s>>>(g, a, runs);
   else
