@@ -255,11 +255,60 @@ def test_bf16_fanout_decode_sixteen_agents(gpu_available):
     shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
                              base.head_dim, base.block_size, "bf16")
     tw = Twin(shape, n_blocks=200, max_pos=1200, max_states=24, wl="fan16", check_kv=False)
-    root = tw.materialize(1030)                    # chunks of 512 keys: 3 chunks
+    root = tw.materialize(1030)                    # chunks of 1024 keys: 2 chunks
     kids = tw.fork(root, 16)
     tw.attend(kids, 7)                             # copy-on-write of the shared tail
     for _ in range(2):
         tw.attend(kids, 1)
     tw.attend(kids[3:9], 1)                        # a sub-batch with longer histories
     tw.attend([root] + kids[:2], 1)
+    tw.close()
+
+
+def test_bf16_ragged_edges(gpu_available):
+    """8B-shaped heads, 2 layers, at sizes that leave partial tiles in every
+    kernel: a one-token state (decode-path kernels over a single key),
+    prefills of 33 and 300 tokens (partial 256-row projection and 64-token
+    attention tiles), decode batches of 3, 5 and 17 (17 agents x 4 query heads
+    is beyond the MFMA decode path: portable kernels at the real head shape,
+    and 17 token rows for the projection), appends of 2 x 33 rows and of 70
+    rows behind 301 cached tokens, a three-segment compose and a pack / unpack
+    of the result."""
+    base = synth.LLAMA8B_SHAPE
+    shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
+                             base.head_dim, base.block_size, "bf16")
+    tw = Twin(shape, n_blocks=220, max_pos=700, max_states=40, wl="ragged")
+    one = tw.materialize(1)
+    a = tw.materialize(33, pos0=5)
+    b = tw.materialize(300)
+    tw.attend([one, a, b], 1)
+    kids = tw.fork(b, 17)
+    tw.attend(kids, 1)                             # copy-on-write of b's partial tail
+    tw.attend(kids[:5], 1)
+    tw.attend([a, one], 33)
+    tw.attend(kids[5:7], 70)
+    c = tw.compose([(one, 0, 2), (a, 3, 30), (kids[0], 100, 302)])
+    tw.attend([c], 1)
+    nb = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
+    hdr, ohdr, buf, pay = tw.pack(c, 0, nb)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.close()
+
+
+def test_api_maxima_on_device(gpu_available):
+    """The largest calls the interface accepts: a fork into KV_MAX_FORK
+    children, one attend over a batch of KV_MAX_BATCH states (each one
+    copy-on-writes the shared partial tail), a compose of KV_MAX_SEGMENTS
+    one-token segments with distinct shifts."""
+    assert kv.KV_MAX_FORK == kv.KV_MAX_BATCH == kv.KV_MAX_SEGMENTS == 64
+    tw = Twin(small_shape(B=4), n_blocks=200, max_pos=128, max_states=80, wl="max")
+    root = tw.materialize(10)
+    kids = tw.fork(root, kv.KV_MAX_FORK)
+    tw.attend(kids, 1)
+    c = tw.compose([(k, 10, 11) for k in kids[:kv.KV_MAX_SEGMENTS]])
+    tw.attend([c], 2)
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_fork(tw.gpu.h, root, kv.KV_MAX_FORK + 1)
+    assert e.value.status in (kv.KV_ERR_ARG, kv.KV_ERR_CAPACITY)
+    kv.kv_sync(tw.gpu.h)
     tw.close()
