@@ -7,6 +7,8 @@ import os
 
 from paper_2607_10987_amd import kvstate as kv
 
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
 
 def test_library_exports_header_symbols():
     lib = kv.lib()
@@ -46,3 +48,14 @@ def test_host_only_calls():
 
 def test_library_path_in_tree():
     assert os.path.dirname(kv.LIB_PATH).endswith("paper_2607_10987_amd")
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU; asking for more exits with a message."""
+    import json
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
