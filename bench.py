@@ -334,7 +334,7 @@ def checkpoint_sweep(args, kv, torch, synth):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "this benchmark measures one GPU; --gpus must be 1"}))
         sys.exit(2)
     import torch
     import synth
