@@ -331,6 +331,257 @@ def checkpoint_sweep(args, kv, torch, synth):
 
 # ------------------------------------------------------------------ main
 
+class Plan:
+    """One workload's step on the device: inputs and pool, the step itself,
+    and its algorithmic work per kernel kind."""
+
+    def __init__(self):
+        self.info = {}
+
+
+def build_plan(wl, args, kv, torch, synth, dev):
+    s = wl.shape
+    L, d, cols, B = s.n_layers, s.d_model, s.qkv_cols, s.block_size
+    HD = s.n_q_heads * s.head_dim
+    tdt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
+    ndec = wl.decode if args.decode is None else args.decode
+    kvb = kv_bytes_per_token(s)
+    w_bytes = L * cols * d * s.elt_bytes
+    pl = Plan()
+    pl.shape = s
+
+    def weights():
+        w = torch.empty((L, cols, d), dtype=tdt, device=dev)
+        for layer in range(L):
+            w[layer] = synth.normal_torch(synth.w_key(args.seed, wl.name, layer), (cols, d),
+                                          s.w_std, s.dtype, dev)
+        return w
+
+    def xin(tag, shape):
+        return synth.normal_torch(synth.x_key(args.seed, wl.name, tag), shape, 1.0, s.dtype, dev)
+
+    def dec_work(batch, keys_per_step):
+        """decode projection and attention bytes over steps with the given
+        unique key counts (a shared block read once per step)"""
+        bq = sum(w_bytes + batch * d * s.elt_bytes + batch * L * cols * s.elt_bytes
+                 for _ in keys_per_step)
+        ba = sum(kvb * k + batch * L * HD * s.elt_bytes * 2 for k in keys_per_step)
+        return bq, ba
+
+    if wl.name == "fanout16-8b":
+        # a 32768-token context, pinned, forked to 16 agents with 1024-token
+        # suffixes; batched decode; then LRU churn: each round evicts down to
+        # 75% of the allocated blocks and refills 12 agents with fresh suffixes
+        ctx, A, suf = wl.context, wl.agents, wl.suffix
+        rounds = wl.extra["evict_rounds"]
+        frac = wl.extra["evict_frac"]
+        refill = int(round(A * (1 - frac)))
+        max_pos = ctx + suf + ndec + 64
+        n_blocks = ctx // B + 1 + (A + refill) * ((suf + ndec) // B + 2) + 64
+        cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, max_pos,
+                          2 * A + 8, s.rope_base, 1)
+        pl.pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, max(ctx, A * suf), A, max_pos))
+        pl.w = weights()
+        pl.pool.set_weights(pl.w, cols * d)
+        x_ctx, x_suf = xin(0, (ctx, d)), xin(1, (A, suf, d))
+        x_dec = xin(2, (ndec, A, 1, d))
+        o_ctx = torch.empty((L, ctx, HD), dtype=tdt, device=dev)
+        o_suf = torch.empty((L, A, suf, HD), dtype=tdt, device=dev)
+        o_dec = torch.empty((L, A, 1, HD), dtype=tdt, device=dev)
+        x_ref = xin(3, (refill, suf, d))
+        o_ref = torch.empty((L, refill, suf, HD), dtype=tdt, device=dev)
+        h = pl.pool.h
+
+        def step():
+            root = kv.kv_materialize(h, x_ctx, ctx, 0, o_ctx)
+            kv.kv_pin(h, root, True)
+            kids = kv.kv_fork(h, root, A)
+            kv.kv_attend(h, kids, x_suf, suf, o_suf)
+            for i in range(ndec):
+                kv.kv_attend(h, kids, x_dec[i], 1, o_dec)
+            freed = []
+            for _ in range(rounds):
+                before = kv.kv_pool_counts(h)
+                alloc = n_blocks - before["free_blocks"]
+                kv.kv_evict(h, int(alloc * (1 - frac)), 0.0, 0.0, 1.0)
+                freed.append(kv.kv_pool_counts(h)["free_blocks"] - before["free_blocks"])
+                new = kv.kv_fork(h, root, refill)
+                kv.kv_attend(h, new, x_ref, suf, o_ref)
+            kv.kv_pin(h, root, False)
+            kv.kv_evict(h, 0, 0.0, 0.0, 1.0)
+            pl.info["freed_per_round"] = freed
+
+        pl.step = step
+        f_mat = proj_flops(s, ctx) + attn_flops(s, 0, ctx)
+        f_app = (A + refill * rounds) * (proj_flops(s, suf) + attn_flops(s, ctx, suf))
+        f_dec = sum(A * (proj_flops(s, 1) + attn_flops(s, ctx + suf + i, 1)) for i in range(ndec))
+        pl.flops = f_mat + f_app + f_dec
+        bq, ba = dec_work(A, [ctx + A * (suf + i + 1) for i in range(ndec)])
+        pl.work = {"qkv": (proj_flops(s, ctx) + (A + refill * rounds) * proj_flops(s, suf), "mfma"),
+                   "attn": (attn_flops(s, 0, ctx) + (A + refill * rounds) * attn_flops(s, ctx, suf),
+                            "mfma"),
+                   "qkv_decode": (bq, "hbm"), "attn_decode": (ba, "hbm")}
+        pl.desc = (f"{wl.name}: context {ctx} (pinned) forked to {A}, append {suf} each, "
+                   f"decode {ndec} (batch {A}), then {rounds} LRU rounds evicting to "
+                   f"{int(100 * (1 - frac))}% of the allocated blocks and refilling {refill} agents "
+                   f"with {suf}-token suffixes")
+        pl.batch, pl.seq = A, ctx + suf + ndec
+        pl.evict_calls = rounds + 1
+        return pl
+
+    if wl.name == "compose8-8b":
+        # 8 agents hold 4096-token segments at positions 0..4095; compose them
+        # into one 32768-token cache (keys re-rotated by 4096 k), append 2048,
+        # decode
+        seg, A, suf = wl.context, wl.agents, wl.suffix
+        N = seg * A
+        max_pos = N + suf + ndec + 64
+        n_blocks = 2 * N // B + (suf + ndec) // B + 64
+        cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, max_pos,
+                          A + 4, s.rope_base, 1)
+        pl.pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, max(seg, suf), 1, max_pos))
+        pl.w = weights()
+        pl.pool.set_weights(pl.w, cols * d)
+        x_seg = [xin(10 + j, (seg, d)) for j in range(A)]
+        x_app, x_dec = xin(1, (1, suf, d)), xin(2, (ndec, 1, 1, d))
+        o_seg = torch.empty((L, seg, HD), dtype=tdt, device=dev)
+        o_app = torch.empty((L, 1, suf, HD), dtype=tdt, device=dev)
+        o_dec = torch.empty((L, 1, 1, HD), dtype=tdt, device=dev)
+        h = pl.pool.h
+
+        def step():
+            agents = [kv.kv_materialize(h, x_seg[j], seg, 0, o_seg) for j in range(A)]
+            c = kv.kv_compose(h, [(a, 0, seg) for a in agents])
+            kv.kv_attend(h, [c], x_app, suf, o_app)
+            for i in range(ndec):
+                kv.kv_attend(h, [c], x_dec[i], 1, o_dec)
+            kv.kv_evict(h, 0, 0.0, 0.0, 1.0)
+
+        pl.step = step
+        f_mat = A * (proj_flops(s, seg) + attn_flops(s, 0, seg))
+        f_app = proj_flops(s, suf) + attn_flops(s, N, suf)
+        f_dec = sum(proj_flops(s, 1) + attn_flops(s, N + suf + i, 1) for i in range(ndec))
+        pl.flops = f_mat + f_app + f_dec
+        bq, ba = dec_work(1, [N + suf + i + 1 for i in range(ndec)])
+        pl.work = {"qkv": (A * proj_flops(s, seg) + proj_flops(s, suf), "mfma"),
+                   "attn": (A * attn_flops(s, 0, seg) + attn_flops(s, N, suf), "mfma"),
+                   "qkv_decode": (bq, "hbm"), "attn_decode": (ba, "hbm"),
+                   "compose_copy": (2 * (A - 1) * (seg // B) * s.block_bytes, "hbm")}
+        pl.desc = (f"{wl.name}: {A} agents materialize {seg}-token segments at positions 0..{seg - 1}, "
+                   f"compose into {N} tokens (segments 1..{A - 1} re-rotated), append {suf}, "
+                   f"decode {ndec}")
+        pl.batch, pl.seq = 1, N + suf + ndec
+        pl.evict_calls = 1
+        return pl
+
+    if wl.name == "pack70b":
+        # a 16384-token context packed into a transfer buffer and unpacked into
+        # a pool whose free blocks are in a seeded random order; 4-agent fork
+        # and batched decode over the unpacked blocks
+        ctx, A = wl.context, wl.agents
+        nb_ctx = -(-ctx // B)
+        max_pos = ctx + ndec + 64
+        n_blocks = 2 * nb_ctx + A * (ndec // B + 2) + 64
+        cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, max_pos,
+                          A + 4, s.rope_base, 1)
+        perm = synth.permutation(args.seed, wl.name, n_blocks)
+        pl.pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, ctx, A, max_pos),
+                          init_free_order=perm)
+        pl.w = weights()
+        pl.pool.set_weights(pl.w, cols * d)
+        x_ctx, x_dec = xin(0, (ctx, d)), xin(2, (ndec, A, 1, d))
+        o_ctx = torch.empty((L, ctx, HD), dtype=tdt, device=dev)
+        o_dec = torch.empty((L, A, 1, HD), dtype=tdt, device=dev)
+        buf = torch.empty(nb_ctx * s.block_bytes, dtype=torch.uint8, device=dev)
+        h = pl.pool.h
+
+        def step():
+            root = kv.kv_materialize(h, x_ctx, ctx, 0, o_ctx)
+            hdr = kv.kv_pack(h, root, 0, nb_ctx, buf)
+            u = kv.kv_unpack(h, hdr, buf)
+            kv.kv_release(h, root)
+            kids = kv.kv_fork(h, u, A)
+            for i in range(ndec):
+                kv.kv_attend(h, kids, x_dec[i], 1, o_dec)
+            kv.kv_evict(h, 0, 0.0, 0.0, 1.0)
+
+        pl.step = step
+        f_mat = proj_flops(s, ctx) + attn_flops(s, 0, ctx)
+        f_dec = sum(A * (proj_flops(s, 1) + attn_flops(s, ctx + i, 1)) for i in range(ndec))
+        pl.flops = f_mat + f_dec
+        bq, ba = dec_work(A, [ctx + A * (i + 1) for i in range(ndec)])
+        pl.work = {"qkv": (proj_flops(s, ctx), "mfma"), "attn": (attn_flops(s, 0, ctx), "mfma"),
+                   "qkv_decode": (bq, "hbm"), "attn_decode": (ba, "hbm"),
+                   "pack": (2 * nb_ctx * s.block_bytes, "hbm"),
+                   "unpack": (2 * nb_ctx * s.block_bytes, "hbm")}
+        pl.desc = (f"{wl.name}: context {ctx} ({nb_ctx} blocks of {s.block_bytes / 2**20:.0f} MiB) "
+                   f"packed and unpacked into a randomly ordered pool, fork {A}, decode {ndec}")
+        pl.batch, pl.seq = A, ctx + ndec
+        pl.evict_calls = 1
+        return pl
+
+    # fork workloads (tiny, fork4-8b): every operator once
+    ctx, A, suf = wl.context, wl.agents, wl.suffix
+    cont = suf + ndec                                   # tokens each agent adds
+    n_comp = ctx + A * cont                             # composed state length
+    max_pos = n_comp + 64
+    blocks_needed = (ctx // B + 1) + A * (cont // B + 2) + 2 * (n_comp // B + 2)
+    n_blocks = blocks_needed + 64
+    cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, max_pos, 64,
+                      s.rope_base, 1)
+    pl.pool = kv.Pool(cfg, n_blocks, kv.kv_scratch_bytes(cfg, max(ctx, A * suf), A, max_pos))
+    pl.w = weights()
+    pl.pool.set_weights(pl.w, cols * d)
+    x_ctx, x_suf = xin(0, (ctx, d)), xin(1, (A, suf, d))
+    x_dec = xin(2, (ndec, A, 1, d))
+    o_ctx = torch.empty((L, ctx, HD), dtype=tdt, device=dev)
+    o_suf = torch.empty((L, A, suf, HD), dtype=tdt, device=dev)
+    o_dec = torch.empty((L, A, 1, HD), dtype=tdt, device=dev)
+    nb_comp = -(-n_comp // B)
+    pack_buf = torch.empty(nb_comp * s.block_bytes, dtype=torch.uint8, device=dev)
+    h = pl.pool.h
+
+    def step():
+        root = kv.kv_materialize(h, x_ctx, ctx, 0, o_ctx)
+        kids = kv.kv_fork(h, root, A)
+        if suf:
+            kv.kv_attend(h, kids, x_suf, suf, o_suf)
+        for i in range(ndec):
+            kv.kv_attend(h, kids, x_dec[i], 1, o_dec)
+        segs = [(root, 0, ctx)] + [(k, ctx, ctx + cont) for k in kids]
+        c = kv.kv_compose(h, segs)
+        nb = kv.kv_state_info(h, c)["n_blocks"]
+        hdr = kv.kv_pack(h, c, 0, nb, pack_buf)
+        kv.kv_unpack(h, hdr, pack_buf)
+        pl.info["nb_comp"] = nb
+        kv.kv_evict(h, 0, 0.0, 0.0, 1.0)
+
+    pl.step = step
+    f_mat = proj_flops(s, ctx) + attn_flops(s, 0, ctx)
+    f_app = A * (proj_flops(s, suf) + attn_flops(s, ctx, suf))
+    f_dec = sum(A * (proj_flops(s, 1) + attn_flops(s, ctx + suf + i, 1)) for i in range(ndec))
+    pl.flops = f_mat + f_app + f_dec
+    bq, ba = dec_work(A, [ctx + A * (suf + i + 1) for i in range(ndec)])
+    copied = A - 1                                        # agent 1's blocks are aliased
+    pl.work = {"qkv": (proj_flops(s, ctx) + A * proj_flops(s, suf), "mfma"),
+               "attn": (attn_flops(s, 0, ctx) + A * attn_flops(s, ctx, suf), "mfma"),
+               "qkv_decode": (bq, "hbm"), "attn_decode": (ba, "hbm"),
+               "compose_copy": (2 * copied * (cont // B) * s.block_bytes, "hbm"),
+               "pack": (2 * nb_comp * s.block_bytes, "hbm"),
+               "unpack": (2 * nb_comp * s.block_bytes, "hbm")}
+    pl.desc = (f"{wl.name}: {L} layers, d_model {d}, {s.n_q_heads}/{s.n_kv_heads} heads, "
+               f"head_dim {s.head_dim}, block {B}; context {ctx}, fork {A}, append {suf}, "
+               f"decode {ndec}, compose {n_comp} tokens, pack/unpack {nb_comp} blocks, evict all")
+    pl.batch, pl.seq = A, n_comp
+    pl.evict_calls = 1
+    return pl
+
+
+NAMES = {"qkv": "materialize+append qkv", "attn": "materialize+append attention",
+         "qkv_decode": "decode qkv", "attn_decode": "decode attention", "compose_copy": "compose",
+         "pack": "pack", "unpack": "unpack"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -351,42 +602,14 @@ def main():
         return
     wl = synth.WORKLOADS[args.workload]
     s = wl.shape
-    ndec = wl.decode if args.decode is None else args.decode
     dev = "cuda"
-    tdt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
-    L, d, cols = s.n_layers, s.d_model, s.qkv_cols
-    ctx, A, suf, B = wl.context, wl.agents, wl.suffix, s.block_size
-    cont = suf + ndec                                   # tokens each agent adds
-    n_comp = ctx + A * cont                             # composed state length
-    max_pos = n_comp + 64
-    blocks_needed = (ctx // B + 1) + A * (cont // B + 2) + 2 * (n_comp // B + 2)
-    n_blocks = blocks_needed + 64
     t_setup = time.perf_counter()
-    print(f"[bench] setup {wl.name}: {n_blocks} blocks of {s.block_bytes / 2**20:.1f} MiB",
-          file=sys.stderr, flush=True)
-
-    # inputs, resident in HBM before timing
-    w = torch.empty((L, cols, d), dtype=tdt, device=dev)
-    for layer in range(L):
-        w[layer] = synth.normal_torch(synth.w_key(args.seed, wl.name, layer), (cols, d), s.w_std,
-                                      s.dtype, dev)
-    x_ctx = synth.normal_torch(synth.x_key(args.seed, wl.name, 0), (ctx, d), 1.0, s.dtype, dev)
-    x_suf = synth.normal_torch(synth.x_key(args.seed, wl.name, 1), (A, suf, d), 1.0, s.dtype, dev)
-    x_dec = synth.normal_torch(synth.x_key(args.seed, wl.name, 2), (ndec, A, 1, d), 1.0, s.dtype,
-                               dev)
-    o_ctx = torch.empty((L, ctx, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
-    o_suf = torch.empty((L, A, suf, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
-    o_dec = torch.empty((L, A, 1, s.n_q_heads * s.head_dim), dtype=tdt, device=dev)
-    cfg = kv.make_cfg(L, d, s.n_q_heads, s.n_kv_heads, s.head_dim, B, s.dtype, max_pos, 64,
-                      s.rope_base, 1)
-    scratch = kv.kv_scratch_bytes(cfg, max(ctx, A * suf), A, max_pos)
-    pool = kv.Pool(cfg, n_blocks, scratch)
-    pool.set_weights(w, cols * d)
-    nb_comp = -(-n_comp // B)
-    pack_buf = torch.empty(nb_comp * s.block_bytes, dtype=torch.uint8, device=dev)
+    print(f"[bench] setup {wl.name}", file=sys.stderr, flush=True)
+    pl = build_plan(wl, args, kv, torch, synth, dev)
+    h = pl.pool.h
     torch.cuda.synchronize()
-    print(f"[bench] setup done in {time.perf_counter() - t_setup:.1f} s", file=sys.stderr,
-          flush=True)
+    print(f"[bench] setup done in {time.perf_counter() - t_setup:.1f} s ({pl.pool.n_blocks} blocks "
+          f"of {s.block_bytes / 2**20:.1f} MiB)", file=sys.stderr, flush=True)
 
     # plain device copy of 1 GiB: reference rate for the HBM-bound operators
     # (and, with --copy-calibration, the reference for HBM byte counters)
@@ -403,99 +626,51 @@ def main():
     copy_gbs = 2.0 * (1 << 30) / (min(copy_ms[1:] or copy_ms) / 1e3) / 1e9
     del src, dst
 
-    info = {}
-
-    def step():
-        root = kv.kv_materialize(pool.h, x_ctx, ctx, 0, o_ctx)
-        kids = kv.kv_fork(pool.h, root, A)
-        if suf:
-            kv.kv_attend(pool.h, kids, x_suf, suf, o_suf)
-        for i in range(ndec):
-            kv.kv_attend(pool.h, kids, x_dec[i], 1, o_dec)
-        segs = [(root, 0, ctx)] + [(k, ctx, ctx + cont) for k in kids]
-        c = kv.kv_compose(pool.h, segs)
-        nb = kv.kv_state_info(pool.h, c)["n_blocks"]
-        hdr = kv.kv_pack(pool.h, c, 0, nb, pack_buf)
-        u = kv.kv_unpack(pool.h, hdr, pack_buf)
-        info["nb_comp"] = nb
-        info["u"] = u
-        n_ev = kv.kv_evict(pool.h, 0, 0.0, 0.0, 1.0)
-        info["evicted"] = n_ev
-
     for i in range(args.warmup):
-        step()
+        pl.step()
         print(f"[bench] warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
-    kv.kv_sync(pool.h)
-    kv.kv_profile_enable(pool.h, True)
-    kv.kv_profile_read(pool.h)
+    kv.kv_sync(h)
+    kv.kv_profile_enable(h, True)
+    kv.kv_profile_read(h)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step()
+        pl.step()
         print(f"[bench] step {i + 1}/{args.steps} done", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = kv.kv_profile_read(pool.h)
-    kv.kv_profile_enable(pool.h, False)
-    kv.kv_sync(pool.h)
+    prof = kv.kv_profile_read(h)
+    kv.kv_profile_enable(h, False)
+    kv.kv_sync(h)
     ms_step = (t1 - t0) * 1000.0 / args.steps
     K = args.steps
 
-    # ---- algorithmic work of one step
-    f_mat = proj_flops(s, ctx) + attn_flops(s, 0, ctx)
-    f_app = A * (proj_flops(s, suf) + attn_flops(s, ctx, suf))
-    f_dec = sum(A * (proj_flops(s, 1) + attn_flops(s, ctx + suf + i, 1)) for i in range(ndec))
-    flops = f_mat + f_app + f_dec
-    kvb = kv_bytes_per_token(s)
-    w_bytes = L * cols * d * s.elt_bytes
-    # decode: weights once + unique KV (shared context once, private per agent) + x/o
-    dec_kv_bytes = sum(kvb * (ctx + A * (suf + i + 1)) for i in range(ndec))
-    dec_io = ndec * A * (d + L * s.n_q_heads * s.head_dim) * s.elt_bytes
-    b_qkv_dec = ndec * (w_bytes + A * d * s.elt_bytes + A * L * cols * s.elt_bytes)
-    b_attn_dec = dec_kv_bytes + ndec * A * L * s.n_q_heads * s.head_dim * s.elt_bytes * 2
-    copied = A - 1                                        # agent 1's blocks are aliased
-    b_compose = 2 * copied * (cont // B) * s.block_bytes
-    b_pack = 2 * info["nb_comp"] * s.block_bytes
-    b_unpack = b_pack
-
-    def ms(kind):
-        return prof[kind][1] / K
+    def ms(kinds):
+        return sum(prof[k][1] for k in kinds) / K
 
     ops = {}
-
-    def put(name, kinds, work, unit, peak):
-        t = sum(ms(k) for k in kinds)
-        rate = (work / (t / 1e3) / (1e12 if unit == "TFLOP/s" else 1e9)) if t > 0 else None
-        ops[name] = {"ms": round(t, 4), "rate": None if rate is None else round(rate, 2),
-                     "unit": unit, "frac": None if rate is None else round(rate / peak, 4)}
-
-    put("materialize+append qkv", ["qkv"], proj_flops(s, ctx) + A * proj_flops(s, suf),
-        "TFLOP/s", MFMA_BF16_PEAK_TF)
-    put("materialize+append attention", ["attn"], attn_flops(s, 0, ctx) +
-        A * attn_flops(s, ctx, suf), "TFLOP/s", MFMA_BF16_PEAK_TF)
-    put("decode qkv", ["qkv_decode"], b_qkv_dec, "GB/s", HBM_PEAK_GBS)
-    put("decode attention", ["attn_decode", "merge"], b_attn_dec, "GB/s", HBM_PEAK_GBS)
-    put("compose", ["compose_copy"], b_compose, "GB/s", HBM_PEAK_GBS)
-    put("pack", ["pack"], b_pack, "GB/s", HBM_PEAK_GBS)
-    put("unpack", ["unpack"], b_unpack, "GB/s", HBM_PEAK_GBS)
-    for k in ("decode qkv", "decode attention", "compose", "pack", "unpack"):
-        if ops[k]["rate"] is not None:
-            ops[k]["frac_of_copy"] = round(ops[k]["rate"] / copy_gbs, 4)
-    ops["fork"] = {"us": round(ms("fork") * 1e3, 2)}
-    ops["evict"] = {"us": round(ms("release") * 1e3, 2)}
+    for kind, (work, bound) in pl.work.items():
+        kinds = [kind, "merge"] if kind == "attn_decode" else [kind]
+        t = ms(kinds)
+        if bound == "mfma":
+            rate, unit, peak = (work / (t / 1e3) / 1e12 if t > 0 else None), "TFLOP/s", MFMA_BF16_PEAK_TF
+        else:
+            rate, unit, peak = (work / (t / 1e3) / 1e9 if t > 0 else None), "GB/s", HBM_PEAK_GBS
+        ops[NAMES[kind]] = {"ms": round(t, 4), "rate": None if rate is None else round(rate, 2),
+                            "unit": unit, "frac": None if rate is None else round(rate / peak, 4)}
+        if bound == "hbm" and rate is not None:
+            ops[NAMES[kind]]["frac_of_copy"] = round(rate / copy_gbs, 4)
+    if prof["fork"][0]:
+        ops["fork"] = {"us": round(ms(["fork"]) * 1e3 / (prof["fork"][0] // K), 2),
+                       "calls_per_step": prof["fork"][0] // K}
+    ops["evict"] = {"us": round(ms(["release"]) * 1e3 / max(pl.evict_calls, 1), 2),
+                    "calls_per_step": pl.evict_calls}
+    if "freed_per_round" in pl.info:
+        ops["evict"]["blocks_freed_per_round"] = pl.info["freed_per_round"]
 
     # ---- roofline of the dominant kernel kind (largest summed duration)
-    work_of = {
-        "qkv": (proj_flops(s, ctx) + A * proj_flops(s, suf), "mfma"),
-        "attn": (attn_flops(s, 0, ctx) + A * attn_flops(s, ctx, suf), "mfma"),
-        "qkv_decode": (b_qkv_dec, "hbm"),
-        "attn_decode": (b_attn_dec, "hbm"),
-        "compose_copy": (b_compose, "hbm"),
-        "pack": (b_pack, "hbm"),
-        "unpack": (b_unpack, "hbm"),
-    }
-    dom = max(work_of, key=lambda k: prof[k][1])
-    work, bound = work_of[dom]
+    dom = max(pl.work, key=lambda k: prof[k][1])
+    work, bound = pl.work[dom]
     t_dom = prof[dom][1] / 1e3
     if bound == "mfma":
         achieved, peak, unit = work * K / t_dom / 1e12, MFMA_BF16_PEAK_TF, "TFLOP/s"
@@ -509,7 +684,7 @@ def main():
                 "launches_per_step": prof[dom][0] // K,
                 "avg_launch_ms": round(prof[dom][1] / max(prof[dom][0], 1), 4)}
 
-    value = flops / (ms_step / 1e3) / 1e12
+    value = pl.flops / (ms_step / 1e3) / 1e12
     out = {
         "metric": "compose/pack GB/s (% HBM peak); materialize+attend TFLOP/s (% MFMA peak)",
         "value": round(value, 3),
@@ -523,12 +698,7 @@ def main():
         "vs_baseline": None,
         "dtype": s.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: {s.n_layers} layers, d_model {d}, "
-                               f"{s.n_q_heads}/{s.n_kv_heads} heads, head_dim {s.head_dim}, "
-                               f"block {B}; context {ctx}, fork {A}, append {suf}, "
-                               f"decode {ndec}, compose {n_comp} tokens, pack/unpack "
-                               f"{info['nb_comp']} blocks, evict all",
-                   "global_batch": A, "seq_len": n_comp},
+        "config": {"workload": pl.desc, "global_batch": pl.batch, "seq_len": pl.seq},
         "ops": ops,
         "roofline": roofline,
         "kernel_ms_per_step": {k: round(v[1] / K, 4) for k, v in prof.items() if v[0]},
@@ -537,7 +707,7 @@ def main():
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, args.seed)
-    pool.close()
+    pl.pool.close()
     print(json.dumps(out), flush=True)
 
 
