@@ -121,7 +121,9 @@ typedef struct {
 
 /* Sizes of the caller-provided device areas for a pool of n_blocks blocks.
  * pool_bytes: the block storage; meta_bytes: refcounts, free ring, block
- * tables, the RoPE table and command staging. */
+ * tables, the RoPE tables (cos and sin of every position and frequency, in
+ * two layouts: position-major and grouped by 4 frequencies) and command
+ * staging. */
 kv_status kv_pool_bytes(const kv_model_cfg* cfg, int64_t n_blocks, size_t* pool_bytes,
                         size_t* meta_bytes);
 

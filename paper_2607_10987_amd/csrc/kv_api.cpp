@@ -46,7 +46,7 @@ uint64_t lineage_word(uint64_t kind, uint64_t parent, uint64_t j) {
 }
 
 struct MetaLayout {
-  size_t hdr, rc, ring, tables, rope_cos, rope_sin, cow, cmd, csum, total;
+  size_t hdr, rc, ring, tables, rope_cos, rope_sin, rope_cos_g, rope_sin_g, cow, cmd, csum, total;
 };
 
 MetaLayout meta_layout(const kv_model_cfg& c, int64_t P) {
@@ -64,6 +64,10 @@ MetaLayout meta_layout(const kv_model_cfg& c, int64_t P) {
   m.rope_cos = off;
   off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
   m.rope_sin = off;
+  off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
+  m.rope_cos_g = off;
+  off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
+  m.rope_sin_g = off;
   off = align256(off + (size_t)c.max_pos * (c.head_dim / 2) * 4);
   m.cow = off;
   off = align256(off + KV_MAX_BATCH * sizeof(int2));
@@ -115,6 +119,8 @@ struct kv_pool {
   int32_t* tables = nullptr;
   float* rope_cos = nullptr;
   float* rope_sin = nullptr;
+  float* rope_cos_g = nullptr;
+  float* rope_sin_g = nullptr;
   int2* cow = nullptr;
   int32_t* cmd = nullptr;
   unsigned long long* csum = nullptr;  // kSumSlots (s1, s2) slots, then the result pair
@@ -159,6 +165,8 @@ struct kv_pool {
     g.tables = tables;
     g.rope_cos = rope_cos;
     g.rope_sin = rope_sin;
+    g.rope_cos_g = rope_cos_g;
+    g.rope_sin_g = rope_sin_g;
     g.block_elems = (int64_t)cfg.n_layers * 2 * cfg.n_kv_heads * cfg.block_size * cfg.head_dim;
     g.max_blocks = max_blocks;
     g.L = cfg.n_layers;
@@ -664,6 +672,8 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   p->tables = (int32_t*)(p->meta + p->ml.tables);
   p->rope_cos = (float*)(p->meta + p->ml.rope_cos);
   p->rope_sin = (float*)(p->meta + p->ml.rope_sin);
+  p->rope_cos_g = (float*)(p->meta + p->ml.rope_cos_g);
+  p->rope_sin_g = (float*)(p->meta + p->ml.rope_sin_g);
   p->cow = (int2*)(p->meta + p->ml.cow);
   p->cmd = (int32_t*)(p->meta + p->ml.cmd);
   p->csum = (unsigned long long*)(p->meta + p->ml.csum);
@@ -682,6 +692,14 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
       sn[pos * half + i] = (float)std::sin(a);
     }
   }
+  // the same values grouped by 4 channels, position-major within a group
+  std::vector<float> csg(cs.size()), sng(sn.size());
+  for (int64_t pos = 0; pos < cfg->max_pos; ++pos)
+    for (int i = 0; i < half; ++i) {
+      const size_t k = ((size_t)(i / 4) * cfg->max_pos + pos) * 4 + i % 4;
+      csg[k] = cs[pos * half + i];
+      sng[k] = sn[pos * half + i];
+    }
   DevHeader h;
   std::memset(&h, 0, sizeof(h));
   h.head = 0;
@@ -693,6 +711,8 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
       hipMemcpyAsync(p->ring, order.data(), n_blocks * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipMemcpyAsync(p->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipMemcpyAsync(p->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->rope_cos_g, csg.data(), csg.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(p->rope_sin_g, sng.data(), sng.size() * 4, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     st = KV_ERR_HIP;
   if (st != KV_OK) {

@@ -13,8 +13,11 @@
 // Kernels, by token count M of the call:
 //   M > 32   k_qkv_dl: 256 channels (2 heads) x 256 tokens per workgroup,
 //            eight waves of 128 x 64, direct global->LDS copies, RoPE in
-//            registers, bf16 tile restaged through LDS so that the final
-//            Q / K / V stores are 16-byte, row-contiguous writes (k_qkv_mfma
+//            registers (factors read from a copy of the table grouped by 4
+//            frequencies, position-major within a group, so that one load
+//            instruction reads consecutive positions), bf16 tile restaged
+//            through LDS so that the final Q / K / V stores are 16-byte,
+//            row-contiguous writes (k_qkv_mfma
 //            with register-staged LDS tiles when d is not a multiple of 64);
 //   M <= 16  k_qkv_decode_dma: weight streaming through per-wave LDS buffers
 //            filled by whole-cache-line copies, token rows staged in LDS
@@ -393,54 +396,78 @@ k_qkv_dl(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict_
                                                               acc[i][j], 0, 0, 0);
     }
   }
-  __syncthreads();
-
   const int half = kDh / 2;
-  uint16_t* S = smem;
   const int hh = (n0 + ch0) / kDh;
   const bool rot = hh < g.Hq + g.Hkv;
-#pragma unroll
-  for (int j = 0; j < TJ; ++j) {
-    const int tl = tk0 + j * 32 + (lane & 31);
-    const int row = m0 + tl;
+  const int64_t gstride = (int64_t)g.max_pos * 4;
+  // RoPE factors of token sub-tile j from the channel-group-major tables (one
+  // load instruction reads 32 consecutive positions of a group: 512
+  // contiguous bytes per half-wave); sub-tile 0's are requested before the
+  // barrier, so that their latency overlaps the last products
+  auto fetch = [&](int j, float4* cf, float4* sf) {
+    const int row = m0 + tk0 + j * 32 + (lane & 31);
     const int pos = row < M ? row_info(a, row).pos : 0;
-    const float* cr = g.rope_cos + (int64_t)pos * half;
-    const float* sr = g.rope_sin + (int64_t)pos * half;
+    const float* cr = g.rope_cos_g + (int64_t)pos * 4;
+    const float* sr = g.rope_sin_g + (int64_t)pos * 4;
 #pragma unroll
-    for (int i = 0; i < TI / 2; ++i) {
-#pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int f0 = i * 32 + e4 * 8 + hl * 4;
-        float4 cs = make_float4(1.f, 1.f, 1.f, 1.f), sn = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (rot) {
-          cs = *(const float4*)(cr + f0);
-          sn = *(const float4*)(sr + f0);
-        }
-        float xr[4], yr[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float xv = acc[i][j][e4 * 4 + q], yv = acc[i + 2][j][e4 * 4 + q];
-          const float c = (&cs.x)[q], s = (&sn.x)[q];
-          xr[q] = xv * c - yv * s;
-          yr[q] = xv * s + yv * c;
-        }
-        *(uint2*)(S + tl * SLD + ch0 + f0) =
-            make_uint2(pack_bf16x2(xr[0], xr[1]), pack_bf16x2(xr[2], xr[3]));
-        *(uint2*)(S + tl * SLD + ch0 + half + f0) =
-            make_uint2(pack_bf16x2(yr[0], yr[1]), pack_bf16x2(yr[2], yr[3]));
+    for (int k = 0; k < 8; ++k) {
+      const int f0 = (k >> 2) * 32 + (k & 3) * 8 + hl * 4;
+      cf[k] = make_float4(1.f, 1.f, 1.f, 1.f);
+      sf[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (rot) {
+        cf[k] = *(const float4*)(cr + (f0 >> 2) * gstride);
+        sf[k] = *(const float4*)(sr + (f0 >> 2) * gstride);
       }
     }
-  }
+  };
+  uint16_t* S = smem;
+  auto rotate = [&](int j, const float4* cf, const float4* sf) {
+    const int tl = tk0 + j * 32 + (lane & 31);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = k >> 2, e4 = k & 3;
+      const int f0 = i * 32 + e4 * 8 + hl * 4;
+      float xr[4], yr[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float xv = acc[i][j][e4 * 4 + q], yv = acc[i + 2][j][e4 * 4 + q];
+        const float c = (&cf[k].x)[q], s = (&sf[k].x)[q];
+        xr[q] = fmaf(xv, c, -(yv * s));
+        yr[q] = fmaf(xv, s, yv * c);
+      }
+      *(uint2*)(S + tl * SLD + ch0 + f0) =
+          make_uint2(pack_bf16x2(xr[0], xr[1]), pack_bf16x2(xr[2], xr[3]));
+      *(uint2*)(S + tl * SLD + ch0 + half + f0) =
+          make_uint2(pack_bf16x2(yr[0], yr[1]), pack_bf16x2(yr[2], yr[3]));
+    }
+  };
+  static_assert(TJ == 2 && TI == 4, "epilogue tiling");
+  float4 c0[8], s0[8], c1[8], s1[8];
+  fetch(0, c0, s0);
   __syncthreads();
+
+  rotate(0, c0, s0);
+  fetch(1, c1, s1);
+  rotate(1, c1, s1);
+  __syncthreads();
+  // coalesced stores: thread tid writes 16-byte chunk tid % G8 of rows
+  // tid / G8 + k (kDlThreads / G8); all destinations (block-table lookups for
+  // K / V rows) are resolved before the first store
   constexpr int G8 = CH / 8;
-  for (int q = tid; q < BT * G8; q += kDlThreads) {
-    const int r = q / G8, c8 = q % G8;
-    const int row = m0 + r;
-    if (row >= M) continue;
-    const uint4 v = *(const uint4*)(S + r * SLD + c8 * 8);
-    const int ch = n0 + c8 * 8;
-    *(uint4*)dest(g, a, qbuf, lc, l, M, row, ch / kDh, ch % kDh) = v;
+  constexpr int NIT = BT * G8 / kDlThreads;
+  constexpr int RSTEP = kDlThreads / G8;
+  static_assert(kDlThreads % G8 == 0 && (BT * G8) % kDlThreads == 0, "store tiling");
+  const int c8 = tid % G8, r0 = tid / G8;
+  const int ch = n0 + c8 * 8;
+  uint16_t* dps[NIT];
+#pragma unroll
+  for (int k = 0; k < NIT; ++k) {
+    const int row = m0 + r0 + k * RSTEP;
+    dps[k] = row < M ? dest(g, a, qbuf, lc, l, M, row, ch / kDh, ch % kDh) : nullptr;
   }
+#pragma unroll
+  for (int k = 0; k < NIT; ++k)
+    if (dps[k] != nullptr) *(uint4*)dps[k] = *(const uint4*)(S + (r0 + k * RSTEP) * SLD + c8 * 8);
 }
 
 typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));

@@ -27,6 +27,8 @@ struct PoolGeom {
   const int32_t* tables;  // [max_states][max_blocks]
   const float* rope_cos;  // [max_pos][dh/2]
   const float* rope_sin;  // [max_pos][dh/2]
+  const float* rope_cos_g;  // [dh/8][max_pos][4]: channels 4q .. 4q+3 of group q
+  const float* rope_sin_g;  // [dh/8][max_pos][4]
   int64_t block_elems;    // L * 2 * Hkv * B * dh
   int32_t max_blocks;
   int32_t L, Hq, Hkv, dh, B, d;
