@@ -3,7 +3,8 @@
 //
 // Forked agents share the blocks of their common context (same physical ids
 // in their block tables).  The keys of a decode step are cut into chunks of
-// kCK positions.  k_decode_plan (one wavefront per chunk) groups the batch
+// ck positions (1024, or 512 for a batch of one, whose chunks are its only
+// source of parallelism: +5-10% there).  k_decode_plan (one wavefront per chunk) groups the batch
 // members whose key counts and block ids agree over the chunk; each group of
 // a chunk is one work unit.  The grouping is the same for every layer and KV
 // head, so it is computed once per call.
@@ -32,7 +33,7 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 #define KV_LDS4(p) ((__attribute__((address_space(3))) v4s*)(p))
 
 constexpr int kDh = 128;
-constexpr int kCK = 1024;              // keys per chunk
+constexpr int kCK = 1024;              // keys per chunk (at most; see decode_ck)
 constexpr int kKT = 32;                // keys per pipeline stage
 constexpr int kStage = 2 * kKT * kDh;  // elements per stage: K rows, then V rows
 constexpr int kPart = kDh + 4;         // floats per partial: m, l, pad, pad, o[128]
@@ -68,23 +69,23 @@ __device__ inline uint32_t pack2(float a, float b) {
   return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
 }
 
-// grid (n_chunks), block 64; dynamic LDS: batch * (kCK / B) ints.
+// grid (n_chunks), block 64; dynamic LDS: batch * (ck / B) ints.
 // Writes the units of chunk c to units[c * batch ...] and their number to
 // n_units[c].
 __global__ void __launch_bounds__(64)
 k_decode_plan(PoolGeom g, AppendDesc a, DecodeUnit* __restrict__ units,
-              int* __restrict__ n_units) {
-  extern __shared__ int s_rows[];  // [batch][kCK / B]: each member's block ids in the chunk
+              int* __restrict__ n_units, int ck) {
+  extern __shared__ int s_rows[];  // [batch][ck / B]: each member's block ids in the chunk
   const int lane = threadIdx.x, c = blockIdx.x, b = a.batch;
-  const int c0 = c * kCK;
-  const int nbc = kCK >> g.b_shift, nbs = __builtin_ctz(nbc);
+  const int c0 = c * ck;
+  const int nbc = ck >> g.b_shift, nbs = __builtin_ctz(nbc);
   const int jb0 = c0 >> g.b_shift;
   for (int i = lane; i < b * nbc; i += 64) {
     const int m = i >> nbs, jb = jb0 + (i & (nbc - 1));
     const int n = a.seq[m].n_before + 1;
     s_rows[i] = (jb << g.b_shift) < n ? g.tables[(int64_t)a.seq[m].slot * g.max_blocks + jb] : -1;
   }
-  const int nk_l = lane < b ? max(0, min(kCK, a.seq[lane].n_before + 1 - c0)) : 0;
+  const int nk_l = lane < b ? max(0, min(ck, a.seq[lane].n_before + 1 - c0)) : 0;
   __syncthreads();
   // lane q describes group q: leader, key count, first block id, members
   int n_groups = 0, g_lead = 0, g_nk = 0, g_first = 0;
@@ -155,7 +156,7 @@ template <int RT, int S>
 __global__ void __launch_bounds__(64)
 k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                 const DecodeUnit* __restrict__ units, const int* __restrict__ n_units,
-                float* __restrict__ part, int n_chunks, int l0, float qk_scale_log2) {
+                float* __restrict__ part, int n_chunks, int ck, int l0, float qk_scale_log2) {
   static_assert(S >= 2 && S <= 4, "stages");
   __shared__ __attribute__((aligned(16))) uint16_t smem[S * kStage];
   const int lane = threadIdx.x, hl = lane >> 5, col = lane & 31;
@@ -187,7 +188,7 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                           (uint32_t)__builtin_amdgcn_readfirstlane(up->mask_lo);
     const int R = __popcll(mask) * G;  // query vectors of the unit
     const bool two = RT > 1 && R > 32;
-    const int c0 = c * kCK;
+    const int c0 = c * ck;
     // lane j: block id of the leader's entry j of the chunk (0 past the end)
     const int tbl = (lane << g.b_shift) < nk
                         ? g.tables[(int64_t)a.seq[lead].slot * g.max_blocks +
@@ -380,14 +381,14 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 // Lane i owns output channels 2i, 2i + 1; the chunk weights exp2(m_c - max)
 // are computed once per chunk and broadcast through LDS.
 __global__ void __launch_bounds__(64)
-k_decode_merge(PoolGeom g, AppendDesc a, const float* __restrict__ part, int n_chunks,
+k_decode_merge(PoolGeom g, AppendDesc a, const float* __restrict__ part, int n_chunks, int ck,
                uint16_t* __restrict__ o, int l0) {
   __shared__ float s_w[64];
   const int sh = blockIdx.x, lc = blockIdx.y, lane = threadIdx.x;
   const int s = sh / g.Hq, h = sh % g.Hq;
   const int b = a.batch;
   const int n = a.seq[s].n_before + 1;
-  const int nc = (n + kCK - 1) / kCK;
+  const int nc = (n + ck - 1) / ck;
   const float* pp = part + (((int64_t)lc * b + s) * g.Hq + h) * n_chunks * kPart;
   float mx = -INFINITY;
   for (int c = lane; c < nc; c += 64) mx = fmaxf(mx, pp[(int64_t)c * kPart]);
@@ -432,13 +433,16 @@ k_decode_merge(PoolGeom g, AppendDesc a, const float* __restrict__ part, int n_c
 
 }  // namespace
 
-int decode_chunks(const AppendDesc& a) { return (a.max_keys + kCK - 1) / kCK; }
+// Keys per chunk of a decode call.
+int decode_ck(const AppendDesc& a) { return a.batch == 1 ? kCK / 2 : kCK; }
+
+int decode_chunks(const AppendDesc& a) { return (a.max_keys + decode_ck(a) - 1) / decode_ck(a); }
 
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
   const int G = g.Hq / g.Hkv;
-  // kCK % B == 0 makes B a power of two with at most 64 block ids per chunk
+  // ck % B == 0 with B >= 16 a power of two: at most 64 block ids per chunk
   return dtype == KV_DTYPE_BF16 && g.dh == kDh && a.T == 1 && a.batch * G <= 64 &&
-         kCK % g.B == 0 && g.B >= 16 && g.b_shift >= 0;
+         decode_ck(a) % g.B == 0 && g.B >= 16 && g.b_shift >= 0;
 }
 
 namespace {
@@ -455,21 +459,29 @@ size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a) {
 }
 
 size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_keys) {
-  const int64_t chunks = (max_keys + kCK - 1) / kCK;
-  return (size_t)L * batch * Hq * chunks * kPart * sizeof(float) +
-         (size_t)chunks * batch * sizeof(DecodeUnit) + (size_t)chunks * sizeof(int) + 3 * 256;
+  // calls of any batch up to `batch`: kCK-key chunks, or kCK / 2 for a batch of one
+  size_t worst = 0;
+  for (const int64_t ck : {(int64_t)kCK, (int64_t)kCK / 2}) {
+    const int64_t b = ck == kCK ? batch : 1;
+    const int64_t chunks = (max_keys + ck - 1) / ck;
+    worst = std::max(worst, (size_t)L * b * Hq * chunks * kPart * sizeof(float) +
+                                (size_t)chunks * b * sizeof(DecodeUnit) +
+                                (size_t)chunks * sizeof(int) + 3 * 256);
+  }
+  return worst;
 }
 
 hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
                               void* scratch, int lc, int l0, hipStream_t s) {
   const int G = g.Hq / g.Hkv;
   const int nch = decode_chunks(a);
+  const int ck = decode_ck(a);
   float* part = (float*)scratch;
   DecodeUnit* units = (DecodeUnit*)((char*)scratch + part_bytes(g, a));
   int* n_units = (int*)((char*)units + unit_bytes(a));
   if (l0 == 0) {  // the grouping holds for every layer group of the call
-    const size_t dyn = (size_t)a.batch * (kCK / g.B) * sizeof(int);
-    k_decode_plan<<<nch, 64, dyn, s>>>(g, a, units, n_units);
+    const size_t dyn = (size_t)a.batch * (ck / g.B) * sizeof(int);
+    k_decode_plan<<<nch, 64, dyn, s>>>(g, a, units, n_units, ck);
   }
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
   const int slots = std::min(nch * a.batch, 2 * nch + a.batch);
@@ -480,17 +492,17 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   // than 32 query vectors per unit): two stages, 15% faster than three.
   if (a.batch * G <= 32)
     k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
-                                              nch, l0, sc);
+                                              nch, ck, l0, sc);
   else
     k_decode_stream<2, 2><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
-                                              nch, l0, sc);
+                                              nch, ck, l0, sc);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_merge(const PoolGeom& g, const AppendDesc& a, void* o, const void* part,
                                int l0, int lc, hipStream_t s) {
   dim3 grid(a.batch * g.Hq, lc);
-  k_decode_merge<<<grid, 64, 0, s>>>(g, a, (const float*)part, decode_chunks(a), (uint16_t*)o,
+  k_decode_merge<<<grid, 64, 0, s>>>(g, a, (const float*)part, decode_chunks(a), decode_ck(a), (uint16_t*)o,
                                       l0);
   return hipGetLastError();
 }
