@@ -295,6 +295,24 @@ def test_bf16_ragged_edges(gpu_available):
     tw.close()
 
 
+def test_bf16_decode_batch_one_multichunk(gpu_available):
+    """A batch of one decodes over its keys in 512-key chunks (forked batches
+    use 1024): decode steps over 1030 and 1031 keys span three chunks, the
+    last one ragged, so the split-key partials and their merge are compared
+    with the oracle element by element; a batch of two over the same state
+    and a fork of it takes the 1024-key chunking."""
+    base = synth.LLAMA8B_SHAPE
+    shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
+                             base.head_dim, base.block_size, "bf16")
+    tw = Twin(shape, n_blocks=160, max_pos=1100, max_states=8, wl="chunks")
+    s = tw.materialize(1029)
+    tw.attend([s], 1)
+    tw.attend([s], 1)
+    kid = tw.fork(s, 1)[0]
+    tw.attend([s, kid], 1)
+    tw.close()
+
+
 def test_api_maxima_on_device(gpu_available):
     """The largest calls the interface accepts: a fork into KV_MAX_FORK
     children, one attend over a batch of KV_MAX_BATCH states (each one
