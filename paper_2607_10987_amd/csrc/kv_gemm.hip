@@ -19,11 +19,12 @@
 //            through LDS so that the final Q / K / V stores are 16-byte,
 //            row-contiguous writes (k_qkv_mfma
 //            with register-staged LDS tiles when d is not a multiple of 64);
-//   M <= 16  k_qkv_decode_pst when the token rows fit in 32 KiB of LDS: one
-//            persistent workgroup per CU streaming the weights of its
-//            (layer, head) tiles through per-wave LDS buffers without a
-//            break between tiles, RoPE in registers;
-//            k_qkv_decode_dma otherwise: weight streaming through per-wave LDS buffers
+//   M <= 16  k_qkv_decode_pst: each workgroup streams the weights of a group
+//            of (layer, head) tiles through per-wave LDS buffers without a
+//            break between tiles, token rows staged once per column chunk,
+//            one accumulator per tile, RoPE in registers;
+//            k_qkv_decode_dma when d is not a multiple of 256: weight
+//            streaming through per-wave LDS buffers
 //            filled by whole-cache-line copies, token rows staged in LDS
 //            (k_qkv_decode_lds, weights loaded straight into registers, when
 //            the buffers do not fit);
@@ -781,39 +782,43 @@ k_qkv_decode_dma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __r
 }
 
 
-// Persistent decode-size projection for a small batch (M * d * 2 <= 32 KiB):
-// one workgroup per CU loops over (layer, head) tiles, and the weight stream
+// Decode-size projection, workgroup-per-tile-group form: workgroup b takes
+// `tpw` consecutive (layer, head) tiles (tpw <= kPstTiles, chosen so that the
+// grid fills whole rounds of CUs) and keeps one accumulator per tile in
+// registers.  The token rows are staged in LDS in column chunks of kd (the
+// whole row when it fits in kPstX bytes, with chunk c of row r at slot
+// c ^ (r & 15)); for each chunk the workgroup runs over its tiles, so a chunk
+// is staged once per workgroup rather than once per tile.  The weight stream
 // of k_qkv_decode_dma (2 rows x 512 bytes per non-temporal global->LDS copy,
-// two batches of 16 rows x 512 bytes per wave) runs on across tile borders,
-// so the copies of a tile's first batch are in flight during the previous
-// tile's epilogue.  The token rows are staged in LDS once (they are the same
-// for every layer), with chunk c of row r at chunk slot c ^ 4 (r & 3).  Wave
-// w multiplies weight rows (channels) w * 8 .. w * 8 + 7 and 64 + w * 8 ..
-// 64 + w * 8 + 7 of the head, so that in the 16x16 output layout the RoPE
-// partners of lane l's channels sit in lane l ^ 32; the rotation runs in
+// two batches of 16 rows x 512 bytes per wave) runs on across tile and chunk
+// borders.  Wave w multiplies channels w * 8 .. w * 8 + 7 and their RoPE
+// partners 64 + w * 8 .. 64 + w * 8 + 7, so that in the 16x16 output layout
+// the partners of lane l's values sit in lane l ^ 32: the rotation runs in
 // registers with factors loaded once, and each lane stores its 4 channels of
-// one token (8 bytes).  grid (min(tiles, CUs)), block 512.
-constexpr int kPstXMax = 32 * 1024;
+// one token (8 bytes).  grid (ceil(tiles / tpw)), block 512.
+constexpr int kPstTiles = 8;
+constexpr int kPstX = 32 * 1024;
 
 __global__ void __launch_bounds__(64 * kDecWaves, 1)
 k_qkv_decode_pst(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
-                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0, int n_lc) {
+                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0, int n_lc,
+                 int tpw, int kd) {
   constexpr int RPI = 1024 / (kDmaKB * 64);      // rows per copy instruction
   constexpr int SPR = kDmaKB * 4;                // 16-byte slots per row and batch
   __shared__ __attribute__((aligned(16))) char wbuf[kDecWaves * kDmaBuf * kDmaBatch];
-  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][d], chunk-swizzled
+  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][kd], chunk-swizzled
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
   const int M = a.batch * a.T, d = g.d;
-  const int N = (g.Hq + 2 * g.Hkv) * kDh;
-  const int nt = N / kDh;
-  const int n_tiles = nt * n_lc;
-  const int G = gridDim.x;
-  const int my_tiles = (n_tiles - (int)blockIdx.x + G - 1) / G;
-  if (my_tiles <= 0) return;
-  const int nb = d / (kDmaKB * 32);
-  const int total = my_tiles * nb;
+  const int nt = g.Hq + 2 * g.Hkv;               // head tiles per layer
+  const int t0 = (int)blockIdx.x * tpw;
+  const int my = min(tpw, nt * n_lc - t0);
+  if (my <= 0) return;
+  const int nck = d / kd;                        // token-row chunks
+  const int nbc = kd / (kDmaKB * 32);            // weight batches per tile and chunk
+  const int per_chunk = my * nbc;
+  const int total = nck * per_chunk;
 
   // copy j of a batch: local rows RPI j + lane / SPR; local row r is channel
   // r + w * 8 (+ 56 for r >= 8) of the head
@@ -825,24 +830,20 @@ k_qkv_decode_pst(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __r
     voff[j] = (uint32_t)ch * d * 2 + (sl ^ (r & 15)) * 16;
   }
   const uint32_t lds_w = lds_addr(wbuf) + wave * kDmaBuf * kDmaBatch;
+  // batch q of the stream: chunk, tile, batch within the tile's chunk
   auto issue = [&](int q) {
-    const int k = q / nb, jb = q - k * nb;
-    const int t = (int)blockIdx.x + k * G;
-    const int lc = t / nt, hi = t - lc * nt;
-    const char* sb = (const char*)(w + (int64_t)(l0 + lc) * w_stride + (int64_t)hi * kDh * d) +
-                     (int64_t)jb * kDmaKB * 64;
+    const int ch = q / per_chunk, rem = q - ch * per_chunk;
+    const int k = rem / nbc, jb = rem - k * nbc;
+    const int t = t0 + k;
+    const int lc = t / nt, hh = t - lc * nt;
+    const char* sb = (const char*)(w + (int64_t)(l0 + lc) * w_stride + (int64_t)hh * kDh * d) +
+                     ((int64_t)ch * kd + (int64_t)jb * kDmaKB * 32) * 2;
     const uint32_t ld = lds_w + (q % kDmaBuf) * kDmaBatch;
 #pragma unroll
     for (int j = 0; j < kDmaNI; ++j) lds_dma16_sv_nt(sb, voff[j], ld + j * 1024);
   };
   issue(0);
 
-  // token rows into LDS (once)
-  const int c8n = d / 8;
-  for (int i = tid; i < M * c8n; i += 64 * kDecWaves) {
-    const int r = i / c8n, c = i - r * c8n;
-    *(uint4*)(xs + (int64_t)r * d + ((c ^ ((r & 3) << 2)) * 8)) = *(const uint4*)(x + (int64_t)r * d + c * 8);
-  }
   // per-lane output row: token lr, channels i0 .. i0 + 3 of the x (lane < 32)
   // or y (lane >= 32) half of the head; RoPE factors are the same for every tile
   const bool xok = lr < M;
@@ -859,60 +860,80 @@ k_qkv_decode_pst(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __r
     const int32_t blk = g.tables[(int64_t)ri.slot * g.max_blocks + ri.u / g.B];
     kvrow = (int64_t)blk * g.block_elems + (int64_t)(ri.u % g.B) * kDh;
   }
-  __syncthreads();
 
   const char* wrd = wbuf + wave * kDmaBuf * kDmaBatch + (lr / RPI) * 1024 + (lr % RPI) * SPR * 16;
-  const uint16_t* xr = xs + (xok ? lr : 0) * d;
-  const int xsw = (lr & 3) << 2;
-  for (int k = 0; k < my_tiles; ++k) {
-    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int jb = 0; jb < nb; ++jb) {
-      const int q = k * nb + jb;
-      // the other buffer was read by the products of batch q - 1; a wave's
-      // copies complete in order, kDmaNI per batch
-      if (q + 1 < total) {
-        issue(q + 1);
-        wait_vmcnt<kDmaNI>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      const char* wb = wrd + (q % kDmaBuf) * kDmaBatch;
-      const int cx = jb * kDmaKB * 4;   // first 16-byte chunk of this batch in a token row
+  const uint16_t* xr = xs + (xok ? lr : 0) * kd;
+  const int c8n = kd / 8;
+  floatx4 acc[kPstTiles];
 #pragma unroll
-      for (int u = 0; u < kDmaKB; ++u) {
-        const int c = 4 * u + lg;
-        const uint4 fa = *(const uint4*)(wb + (c ^ lr) * 16);
-        const uint4 fb = xok ? *(const uint4*)(xr + ((cx + c) ^ xsw) * 8) : make_uint4(0, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa),
-                                                      __builtin_bit_cast(bf16x8v, fb), acc, 0, 0,
-                                                      0);
+  for (int k = 0; k < kPstTiles; ++k) acc[k] = floatx4{0.f, 0.f, 0.f, 0.f};
+  int q = 0;
+  for (int ch = 0; ch < nck; ++ch) {
+    // token rows, columns [ch kd, ch kd + kd), into LDS
+    if (ch > 0) __syncthreads();  // every wave has read the previous chunk
+    for (int i = tid; i < M * c8n; i += 64 * kDecWaves) {
+      const int r = i / c8n, c = i - r * c8n;
+      *(uint4*)(xs + (int64_t)r * kd + ((c ^ (r & 15)) * 8)) =
+          *(const uint4*)(x + (int64_t)r * d + (int64_t)ch * kd + c * 8);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kPstTiles; ++k) {
+      if (k < my) {
+        for (int jb = 0; jb < nbc; ++jb, ++q) {
+          // the other buffer was read by the products of batch q - 1; a
+          // wave's copies complete in order, kDmaNI per batch
+          if (q + 1 < total) {
+            issue(q + 1);
+            wait_vmcnt<kDmaNI>();
+          } else {
+            wait_vmcnt<0>();
+          }
+          const char* wb = wrd + (q % kDmaBuf) * kDmaBatch;
+          const int cx = jb * kDmaKB * 4;  // first 16-byte chunk of this batch in a token row
+#pragma unroll
+          for (int u = 0; u < kDmaKB; ++u) {
+            const int c = 4 * u + lg;
+            const uint4 fa = *(const uint4*)(wb + (c ^ lr) * 16);
+            const uint4 fb =
+                xok ? *(const uint4*)(xr + ((cx + c) ^ lr) * 8) : make_uint4(0, 0, 0, 0);
+            acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa),
+                                                             __builtin_bit_cast(bf16x8v, fb),
+                                                             acc[k], 0, 0, 0);
+          }
+        }
       }
     }
-    // epilogue in registers: lane l holds channels 4 (l / 16) + e (local
-    // rows) of token l % 16; local rows 8 .. 15 (lanes 32 .. 63) are the
-    // partners (channel + 64) of rows 0 .. 7 (lanes 0 .. 31)
-    const int t = (int)blockIdx.x + k * G;
-    const int lc = t / nt, hh = t - lc * nt, l = l0 + lc;
-    const bool rot = hh < g.Hq + g.Hkv;
-    float o[4];
+  }
+  // epilogue in registers: lane l holds channels 4 (l / 16) + e (local rows)
+  // of token l % 16; local rows 8 .. 15 (lanes 32 .. 63) are the partners
+  // (channel + 64) of rows 0 .. 7 (lanes 0 .. 31)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[e]), __float_as_uint(acc[e]),
-                                                      false, false);
-      const float xv = __uint_as_float(r[0]), yv = __uint_as_float(r[1]);
-      const float c = (&cs.x)[e], s = (&sn.x)[e];
-      o[e] = !rot ? acc[e] : (lane < 32 ? fmaf(xv, c, -(yv * s)) : fmaf(xv, s, yv * c));
-    }
-    if (xok) {
-      uint16_t* dp;
-      if (hh < g.Hq) {
-        dp = qbuf + (int64_t)lc * M * g.Hq * kDh + qrow + (int64_t)hh * kDh + coff;
-      } else {
-        const int kv = hh < g.Hq + g.Hkv ? 0 : 1;
-        const int gh = hh - g.Hq - kv * g.Hkv;
-        dp = (uint16_t*)g.pool + kvrow + tile_off(g, l, kv, gh, 0) + coff;
+  for (int k = 0; k < kPstTiles; ++k) {
+    if (k < my) {
+      const int t = t0 + k;
+      const int lc = t / nt, hh = t - lc * nt, l = l0 + lc;
+      const bool rot = hh < g.Hq + g.Hkv;
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[k][e]),
+                                                        __float_as_uint(acc[k][e]), false, false);
+        const float xv = __uint_as_float(r[0]), yv = __uint_as_float(r[1]);
+        const float c = (&cs.x)[e], s = (&sn.x)[e];
+        o[e] = !rot ? acc[k][e] : (lane < 32 ? fmaf(xv, c, -(yv * s)) : fmaf(xv, s, yv * c));
       }
-      *(uint2*)dp = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+      if (xok) {
+        uint16_t* dp;
+        if (hh < g.Hq) {
+          dp = qbuf + (int64_t)lc * M * g.Hq * kDh + qrow + (int64_t)hh * kDh + coff;
+        } else {
+          const int kv = hh < g.Hq + g.Hkv ? 0 : 1;
+          const int gh = hh - g.Hq - kv * g.Hkv;
+          dp = (uint16_t*)g.pool + kvrow + tile_off(g, l, kv, gh, 0) + coff;
+        }
+        *(uint2*)dp = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+      }
     }
   }
 }
@@ -938,17 +959,37 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
   // beside the weight buffers
   int kd = g.d;
   while (kd % 512 == 0 && (size_t)M * (kd + 8) * 2 + kDmaStatic > 160 * 1024) kd /= 2;
-  if (M <= 16 && (size_t)M * g.d * 2 <= kPstXMax && g.d % (kDmaKB * 32) == 0) {
+  // token-row chunk of the tile-group kernel: the whole row, else halves, ...
+  int kx = g.d;
+  while ((size_t)M * kx * 2 > kPstX && kx % (2 * kDmaKB * 32) == 0) kx /= 2;
+  if (M <= 16 && g.d % (kDmaKB * 32) == 0 && kx % (kDmaKB * 32) == 0 &&
+      (size_t)M * kx * 2 <= kPstX) {
     static int n_cu[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
     if (n_cu[dev] == 0 &&
         hipDeviceGetAttribute(&n_cu[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return hipErrorInvalidDevice;
-    const int tiles = (N / kDh) * lc;
-    const int grid = tiles < n_cu[dev] ? tiles : n_cu[dev];
-    k_qkv_decode_pst<<<grid, 64 * kDecWaves, (size_t)M * g.d * 2, s>>>(
-        g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0, lc);
+    // tiles per workgroup: the most (up to kPstTiles) whose grid wastes at
+    // most 3% of its last round of CUs, else the least wasteful
+    const int tiles = (g.Hq + 2 * g.Hkv) * lc;
+    int tpw = 1;
+    double best = 2.0;
+    for (int t = kPstTiles; t >= 1; --t) {
+      const int64_t grid = (tiles + t - 1) / t;
+      const int64_t rounds = (grid + n_cu[dev] - 1) / n_cu[dev];
+      const double waste = (double)(rounds * n_cu[dev] - grid) / (double)(rounds * n_cu[dev]);
+      if (waste <= 0.03) {
+        tpw = t;
+        break;
+      }
+      if (waste < best) {
+        best = waste;
+        tpw = t;
+      }
+    }
+    k_qkv_decode_pst<<<(tiles + tpw - 1) / tpw, 64 * kDecWaves, (size_t)M * kx * 2, s>>>(
+        g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0, lc, tpw, kx);
   } else if (M <= 16 && kd % (kDmaKB * 32) == 0 && (size_t)M * (kd + 8) * 2 + kDmaStatic <= 160 * 1024) {
     dim3 grid(N / kDh, 1, lc);
     k_qkv_decode_dma<<<grid, 64 * kDecWaves, (size_t)M * (kd + 8) * 2, s>>>(
