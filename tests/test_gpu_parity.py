@@ -300,7 +300,8 @@ def test_bf16_decode_batch_one_multichunk(gpu_available):
     use 1024): decode steps over 1030 and 1031 keys span three chunks, the
     last one ragged, so the split-key partials and their merge are compared
     with the oracle element by element; a batch of two over the same state
-    and a fork of it takes the 1024-key chunking."""
+    and a fork of it takes the 1024-key chunking, then appends 3 tokens each
+    (6 token rows: the decode-size projection with rows of two sequences)."""
     base = synth.LLAMA8B_SHAPE
     shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
                              base.head_dim, base.block_size, "bf16")
@@ -310,6 +311,7 @@ def test_bf16_decode_batch_one_multichunk(gpu_available):
     tw.attend([s], 1)
     kid = tw.fork(s, 1)[0]
     tw.attend([s, kid], 1)
+    tw.attend([s, kid], 3)      # 6 token rows, 3 per sequence, through the decode-size projection
     tw.close()
 
 
