@@ -226,7 +226,9 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   float m_run = -INFINITY, l_run = 0.f;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  static_assert(kPS >= 3 && kPS <= 4, "stages");
+  // the step below computes QK^T of tile t + 1 before its own barrier, so
+  // tile t + 1 must have been made visible one step earlier: four stages
+  static_assert(kPS == 4, "stages");
   auto wait_tiles = [](int k) {
     if (k >= 2)
       wait_vmcnt<8>();
