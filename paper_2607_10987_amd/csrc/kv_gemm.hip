@@ -32,6 +32,8 @@
 //            tokens, fp32 tile in LDS for the rotation.
 // Q goes to the scratch buffer [lc][M][Hq * dh]; K and V rows go to
 // pool[table[slot][u / B]][l][K|V][kv head][u % B][:] with u = n_before + t.
+#include <atomic>
+
 #include "kv_dma.h"
 #include "kv_fast.h"
 
@@ -964,12 +966,18 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
   while ((size_t)M * kx * 2 > kPstX && kx % (2 * kDmaKB * 32) == 0) kx /= 2;
   if (M <= 16 && g.d % (kDmaKB * 32) == 0 && kx % (kDmaKB * 32) == 0 &&
       (size_t)M * kx * 2 <= kPstX) {
-    static int n_cu[64] = {};
+    // CU count per device, cached (calls from several threads may race to
+    // store the same value)
+    static std::atomic<int> cu_cache[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (n_cu[dev] == 0 &&
-        hipDeviceGetAttribute(&n_cu[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      return hipErrorInvalidDevice;
+    int n_cu = cu_cache[dev].load(std::memory_order_relaxed);
+    if (n_cu <= 0) {
+      if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+          n_cu <= 0)
+        return hipErrorInvalidDevice;
+      cu_cache[dev].store(n_cu, std::memory_order_relaxed);
+    }
     // tiles per workgroup: the most (up to kPstTiles) whose grid wastes at
     // most 3% of its last round of CUs, else the least wasteful
     const int tiles = (g.Hq + 2 * g.Hkv) * lc;
@@ -977,8 +985,8 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
     double best = 2.0;
     for (int t = kPstTiles; t >= 1; --t) {
       const int64_t grid = (tiles + t - 1) / t;
-      const int64_t rounds = (grid + n_cu[dev] - 1) / n_cu[dev];
-      const double waste = (double)(rounds * n_cu[dev] - grid) / (double)(rounds * n_cu[dev]);
+      const int64_t rounds = (grid + n_cu - 1) / n_cu;
+      const double waste = (double)(rounds * n_cu - grid) / (double)(rounds * n_cu);
       if (waste <= 0.03) {
         tpw = t;
         break;
