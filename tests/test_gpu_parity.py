@@ -147,6 +147,29 @@ def test_bf16_llama_shape_two_layers(gpu_available):
     tw.close()
 
 
+def test_bf16_70b_heads_two_layers(gpu_available):
+    """70B-shaped heads (d_model 8192, 64 q / 8 kv heads: 8 query heads per KV
+    head, dh 128, blocks of 32), 2 layers, element by element: a ragged
+    materialize, batched decode of four forks (token rows staged in two
+    column chunks of the decode-size projection), a 40-token append of two
+    of them, a compose and a pack / unpack of it."""
+    base = synth.LLAMA70B_SHAPE
+    shape = synth.ModelShape("70b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
+                             base.head_dim, base.block_size, "bf16")
+    tw = Twin(shape, n_blocks=64, max_pos=512, max_states=12, wl="70b")
+    root = tw.materialize(300)                     # 300 mod 32 = 12: partial tail
+    kids = tw.fork(root, 4)
+    for _ in range(2):
+        tw.attend(kids, 1)
+    tw.attend(kids[:2], 40)
+    c = tw.compose([(root, 0, 300), (kids[0], 300, 342), (kids[3], 300, 302)])
+    tw.attend([c], 1)
+    nb = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
+    hdr, ohdr, buf, pay = tw.pack(c, 0, nb)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.close()
+
+
 def test_pack_unpack_bit_exact_round_trips(gpu_available):
     for dtype in ("f32", "bf16"):
         shape = small_shape(dtype, B=4, dh=32, L=3, hq=4, hkv=2)
