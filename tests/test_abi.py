@@ -59,3 +59,20 @@ def test_bench_refuses_several_gpus():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
+
+
+def test_scratch_bound_covers_decode_partials():
+    """kv_scratch_bytes bounds the decode split-key partials for every batch
+    up to the one asked for: fp32 (m, l, pad, pad, o[dh]) per (layer, member,
+    query head, chunk), chunks of 1024 keys, or of 512 for a batch of one."""
+    c = kv.make_cfg(32, 4096, 32, 8, 128, 16, "bf16", 35072, 64)
+    q_bytes = 32 * 1 * 32 * 128 * 2                # one token row of Q per layer
+    for batch in (1, 2, 4, 16):
+        for keys in (1, 511, 513, 8704, 34816):
+            need = 0
+            for b in range(1, batch + 1):
+                ck = 512 if b == 1 else 1024
+                chunks = -(-keys // ck)
+                need = max(need, 32 * b * 32 * chunks * (4 + 128) * 4)
+            got = kv.kv_scratch_bytes(c, 1, batch, keys)
+            assert got >= need + q_bytes, (batch, keys, got, need)
