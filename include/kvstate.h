@@ -18,9 +18,19 @@
  *   kv_release, kv_evict and kv_evict_truncate synchronise `stream`
  *   before returning.
  * - The caller owns all device memory: the pool, the metadata area, the
- *   scratch area, weights, inputs, outputs and transfer buffers.  Device
- *   pointers must be 256-byte aligned.  The library owns only host-side
- *   catalog memory.
+ *   scratch area, weights, inputs, outputs and transfer buffers.  The pool,
+ *   metadata and scratch areas must be 256-byte aligned, the other buffers
+ *   16-byte aligned.  Every device buffer must be device memory of the GPU
+ *   that was current at kv_pool_create, inside one allocation that holds the
+ *   bytes the call reads or writes: the library checks this before it
+ *   launches anything (KV_ERR_ARG for the wrong kind of memory or a
+ *   misaligned pointer, KV_ERR_BUFSIZE for an allocation that ends too
+ *   early).  The library owns only host-side catalog memory.
+ * - A kernel launch that fails after a call has started changing the pool
+ *   (KV_ERR_HIP) leaves the host catalog as it was before the call, but the
+ *   device may hold part of the call's effect, so the pool is marked failed:
+ *   every later call on it returns KV_ERR_HIP (only kv_pool_destroy and the
+ *   read-only queries still work).
  * - Layouts are row-major.  `dtype` is KV_DTYPE_F32 (float) or KV_DTYPE_BF16
  *   (bfloat16); inputs, weights, outputs and pool contents all use it.
  *
@@ -257,6 +267,15 @@ kv_status kv_state_info(kv_pool* pool, kv_state state, int64_t* pos0, int64_t* n
                         int64_t* n_blocks, uint64_t* lineage, int64_t* state_id);
 kv_status kv_pool_counts(kv_pool* pool, int64_t* free_blocks, int64_t* live_states,
                          int64_t* clock);
+
+/* The terms of a state's KV-Evict score (score = alpha*reuse - beta*size -
+ * gamma*age, KV-Evict algorithm): reuse = number of operator calls that took
+ * the state as an input (fork parent, attend member, compose segment, pack
+ * and checkpoint source), last_access = the pool clock at its last touch (age
+ * = clock - last_access, the clock from kv_pool_counts), pinned = 1 while it
+ * is excluded from eviction.  Any output pointer may be NULL. */
+kv_status kv_state_usage(kv_pool* pool, kv_state state, int64_t* reuse, int64_t* last_access,
+                         int32_t* pinned);
 
 /* Device-side metadata read back (synchronises `stream`): a state's block
  * table (host_out must hold n_blocks entries) and the allocator (refcount and

@@ -107,6 +107,8 @@ static_assert(sizeof(kv_pack_header) == 160, "kv_pack_header layout");
 struct kv_pool {
   kv_model_cfg cfg;
   int64_t P = 0;
+  int device = 0;       // the GPU the pool's memory is on (current at creation)
+  bool failed = false;  // a launch failed after device state changed: refuse further work
   int32_t max_blocks = 0;
   char* pool = nullptr;
   char* meta = nullptr;
@@ -255,6 +257,17 @@ kv_status hip_ok(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_HIP; }
     if (_st != KV_OK) return _st;     \
   } while (0)
 #define KV_HIP(expr) KV_TRY(hip_ok(expr))
+// A kernel launch of a call that changes pool state: if it fails, the device
+// may already hold part of the call's effect while the host catalog does not,
+// so the pool is marked failed and refuses every later operation.
+#define KV_LAUNCH(p, expr)                 \
+  do {                                     \
+    if ((expr) != hipSuccess) {            \
+      (void)hipGetLastError();             \
+      (p)->failed = true;                  \
+      return KV_ERR_HIP;                   \
+    }                                      \
+  } while (0)
 
 // Brackets the kernel launches of one scope with events when profiling is on.
 struct Timed {
@@ -284,7 +297,7 @@ kv_status run_alloc(kv_pool* p, const AllocArgs& a, hipStream_t s) {
   if (need == 0) return KV_OK;
   {
     Timed t(p, KV_KERNEL_ALLOC, s);
-    KV_HIP(launch_alloc(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
+    KV_LAUNCH(p, launch_alloc(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
                         p->head, a, p->cow, s));
   }
   p->head += need;
@@ -304,7 +317,7 @@ kv_status run_release(kv_pool* p, const std::vector<int32_t>& cand, int64_t max_
   KV_HIP(hipMemcpyAsync(p->cmd, cand.data(), cand.size() * 4, hipMemcpyHostToDevice, s));
   {
     Timed t(p, KV_KERNEL_RELEASE, s);
-    KV_HIP(launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
+    KV_LAUNCH(p, launch_release(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks, (int32_t)p->P,
                           p->cmd, n, max_alloc, p->head, p->tail, kept ? 1 : 0,
                           kept ? kept_dev : nullptr, s));
   }
@@ -366,7 +379,7 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
   for (int i = 0; i < aa.n_req; ++i) any_cow |= aa.req[i].cow > 0;
   if (any_cow) {
     Timed t(p, KV_KERNEL_COW, s);
-    KV_HIP(launch_cow(g, c.dtype, p->cow, aa, s));
+    KV_LAUNCH(p, launch_cow(g, c.dtype, p->cow, aa, s));
   }
   void* part = p->scratch + q_layer * lc_max;
   for (int l0 = 0; l0 < c.n_layers; l0 += lc_max) {
@@ -374,21 +387,21 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
     bool done = false;
     {
       Timed t(p, ad.T == 1 ? KV_KERNEL_QKV_DECODE : KV_KERNEL_QKV, s);
-      KV_HIP(launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s,
+      KV_LAUNCH(p, launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s,
                              &done));
       if (!done)
-        KV_HIP(launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
+        KV_LAUNCH(p, launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
     }
     done = false;
     bool merge = false;
     {
       Timed t(p, ad.T == 1 ? KV_KERNEL_ATTN_DECODE : KV_KERNEL_ATTN, s);
-      KV_HIP(launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done, &merge));
-      if (!done) KV_HIP(launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
+      KV_LAUNCH(p, launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done, &merge));
+      if (!done) KV_LAUNCH(p, launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
     }
     if (merge) {
       Timed t(p, KV_KERNEL_MERGE, s);
-      KV_HIP(launch_attn_merge(g, c.dtype, ad, o, part, l0, lc, s));
+      KV_LAUNCH(p, launch_attn_merge(g, c.dtype, ad, o, part, l0, lc, s));
     }
   }
   return KV_OK;
@@ -402,13 +415,14 @@ namespace {
 // device memory as is, pinned host memory (hipHostMalloc) through its device
 // mapping; pageable or unknown host memory is rejected, so that no kernel is
 // ever launched on an address the GPU cannot reach.
-kv_status device_view(const void* p, const void** out) {
+kv_status device_view(const void* p, const void** out, bool* on_device = nullptr) {
   hipPointerAttribute_t a;
   std::memset(&a, 0, sizeof(a));
   if (hipPointerGetAttributes(&a, p) != hipSuccess) {
     (void)hipGetLastError();
     return KV_ERR_ARG;
   }
+  if (on_device) *on_device = a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged;
   if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) {
     *out = p;
     return KV_OK;
@@ -419,6 +433,31 @@ kv_status device_view(const void* p, const void** out) {
     return KV_OK;
   }
   return KV_ERR_ARG;
+}
+
+// A device buffer the kernels of `p` read or write: device (or managed) memory
+// of the pool's GPU, 16-byte aligned, inside an allocation that extends at
+// least `bytes` bytes past it (KV_ERR_BUFSIZE otherwise).  Anything else is
+// rejected before a kernel could be launched on it.
+kv_status device_span(int device, const void* ptr, size_t bytes) {
+  if (!ptr || ((uintptr_t)ptr & 15)) return KV_ERR_ARG;
+  hipPointerAttribute_t a;
+  std::memset(&a, 0, sizeof(a));
+  if (hipPointerGetAttributes(&a, ptr) != hipSuccess) {
+    (void)hipGetLastError();
+    return KV_ERR_ARG;
+  }
+  if ((a.type != hipMemoryTypeDevice && a.type != hipMemoryTypeManaged) || a.device != device)
+    return KV_ERR_ARG;
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)ptr) == hipSuccess && base) {
+    const uintptr_t lo = (uintptr_t)base, q = (uintptr_t)ptr;
+    if (q < lo || q - lo > size || bytes > size - (q - lo)) return KV_ERR_BUFSIZE;
+  } else {
+    (void)hipGetLastError();  // no range known: the type check above stands
+  }
+  return KV_OK;
 }
 
 
@@ -525,14 +564,14 @@ kv_status abort_transfer(kv_pool* p, int32_t slot, hipStream_t s) {
 // Clear the checksum slots (the folding kernel clears what it reads; its
 // result is overwritten by csum_end).
 kv_status csum_begin(kv_pool* p, hipStream_t s) {
-  KV_HIP(launch_csum_final(p->csum, p->csum + 2 * kSumSlots, s));
+  KV_LAUNCH(p, launch_csum_final(p->csum, p->csum + 2 * kSumSlots, s));
   return KV_OK;
 }
 
 // Fold the slots into (s1, s2), clear them, synchronise, return the pair.
 kv_status csum_end(kv_pool* p, hipStream_t s, uint64_t out[2]) {
   unsigned long long* res = p->csum + 2 * kSumSlots;
-  KV_HIP(launch_csum_final(p->csum, res, s));
+  KV_LAUNCH(p, launch_csum_final(p->csum, res, s));
   unsigned long long h[2];
   KV_HIP(hipMemcpyAsync(h, res, sizeof(h), hipMemcpyDeviceToHost, s));
   KV_HIP(hipStreamSynchronize(s));
@@ -644,6 +683,15 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   KV_TRY(check_cfg(cfg));
   if (!out || !pool_dev || !meta_dev || n_blocks < 1 || n_blocks > INT32_MAX) return KV_ERR_ARG;
   if (((uintptr_t)pool_dev | (uintptr_t)meta_dev | (uintptr_t)scratch_dev) & 255) return KV_ERR_ARG;
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) return KV_ERR_HIP;
+  {
+    size_t pb = 0, mb = 0;
+    KV_TRY(kv_pool_bytes(cfg, n_blocks, &pb, &mb));
+    KV_TRY(device_span(device, pool_dev, pb));
+    KV_TRY(device_span(device, meta_dev, mb));
+    if (scratch_dev) KV_TRY(device_span(device, scratch_dev, scratch_bytes));
+  }
   std::vector<int32_t> order(n_blocks);
   if (init_free_order) {
     std::vector<char> seen(n_blocks, 0);
@@ -660,6 +708,7 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   if (!p) return KV_ERR_ARG;
   p->cfg = *cfg;
   p->P = n_blocks;
+  p->device = device;
   p->max_blocks = (int32_t)ceil_div(cfg->max_pos, cfg->block_size);
   p->pool = (char*)pool_dev;
   p->meta = (char*)meta_dev;
@@ -733,7 +782,10 @@ kv_status kv_set_weights(kv_pool* p, const void* w_dev, int64_t layer_stride_ele
   const int64_t per = (int64_t)(p->cfg.n_q_heads + 2 * p->cfg.n_kv_heads) * p->cfg.head_dim *
                       p->cfg.d_model;
   if (layer_stride_elems < per && p->cfg.n_layers > 1) return KV_ERR_ARG;
-  if ((uintptr_t)w_dev & 15) return KV_ERR_ARG;
+  const size_t bytes =
+      (size_t)((p->cfg.n_layers - 1) * std::max<int64_t>(layer_stride_elems, 0) + per) *
+      elt_bytes(p->cfg);
+  KV_TRY(device_span(p->device, w_dev, bytes));
   p->w = w_dev;
   p->w_stride = layer_stride_elems;
   return KV_OK;
@@ -742,9 +794,13 @@ kv_status kv_set_weights(kv_pool* p, const void* w_dev, int64_t layer_stride_ele
 kv_status kv_materialize(kv_pool* p, const void* x_dev, int64_t T, int64_t pos0, void* o_dev,
                          kv_stream stream, kv_state* out) {
   if (!p || !x_dev || !o_dev || !out || T <= 0 || pos0 < 0) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   if (!p->w) return KV_ERR_ARG;
   const kv_model_cfg& c = p->cfg;
   if (pos0 + T > c.max_pos) return KV_ERR_CAPACITY;
+  const size_t elt = elt_bytes(c);
+  KV_TRY(device_span(p->device, x_dev, (size_t)T * c.d_model * elt));
+  KV_TRY(device_span(p->device, o_dev, (size_t)c.n_layers * T * c.n_q_heads * c.head_dim * elt));
   const int32_t slot = p->take_slot();
   if (slot < 0) return KV_ERR_CAPACITY;
   const int64_t nb = ceil_div(T, c.block_size);
@@ -757,17 +813,19 @@ kv_status kv_materialize(kv_pool* p, const void* x_dev, int64_t T, int64_t pos0,
   aa.n_req = 1;
   aa.req[0].slot = slot;
   aa.req[0].count = (int32_t)nb;
+  // the catalog changes only once every launch of the call is enqueued
+  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
   StateRec& r = p->open_state(slot, pos0, T, nb,
                               lineage_word(KV_LINEAGE_MATERIALIZE, kNoParent, 0));
   if (T % c.block_size) r.group = p->new_group(1);
   p->touch(r, false);
-  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
   *out = p->handle(slot);
   return KV_OK;
 }
 
 kv_status kv_fork(kv_pool* p, kv_state parent, int32_t k, kv_state* children, kv_stream stream) {
   if (!p || !children || k < 1 || k > KV_MAX_FORK) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   int32_t ps;
   KV_TRY(p->lookup(parent, &ps));
   if (p->live() + k > p->cfg.max_states) return KV_ERR_CAPACITY;
@@ -789,7 +847,7 @@ kv_status kv_fork(kv_pool* p, kv_state parent, int32_t k, kv_state* children, kv
   if (par.group >= 0) p->holders[par.group] += k;
   {
     Timed t(p, KV_KERNEL_FORK, S(stream));
-    KV_HIP(launch_fork(p->dhdr, p->tables, p->max_blocks, p->rc, fa, S(stream)));
+    KV_LAUNCH(p, launch_fork(p->dhdr, p->tables, p->max_blocks, p->rc, fa, S(stream)));
   }
   p->touch(p->slots[ps], true);
   for (int j = 0; j < k; ++j) {
@@ -803,6 +861,7 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
                     int64_t T, void* o_dev, kv_stream stream) {
   if (!p || !states || !x_dev || !o_dev || batch < 1 || batch > KV_MAX_BATCH || T <= 0)
     return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   if (!p->w) return KV_ERR_ARG;
   for (int i = 0; i < batch; ++i)
     for (int j = 0; j < i; ++j)
@@ -832,6 +891,7 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
     if (shared_tail) left.push_back({r.group, 1});
     aa.req[i].slot = slots[i];
     aa.req[i].cow = shared_tail ? (int32_t)(r.n % B) : 0;
+    aa.req[i].partial = (int32_t)(r.n % B);
     aa.req[i].first = (int32_t)r.nblocks;
     aa.req[i].count = (int32_t)(ceil_div(r.n + T, B) - ceil_div(r.n, B));
     need += aa.req[i].count + (shared_tail ? 1 : 0);
@@ -842,6 +902,12 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
   const AppendDesc ad = make_desc(p, slots, nbef, pos0, T);
   size_t ql, ex;
   if (layers_per_group(p, ad, &ql, &ex) < 1) return KV_ERR_BUFSIZE;
+  const size_t elt = elt_bytes(c);
+  KV_TRY(device_span(p->device, x_dev, (size_t)batch * T * c.d_model * elt));
+  KV_TRY(device_span(p->device, o_dev,
+                     (size_t)c.n_layers * batch * T * c.n_q_heads * c.head_dim * elt));
+  // the catalog changes only once every launch of the call is enqueued
+  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
   for (int i = 0; i < batch; ++i) {
     StateRec& r = p->slots[slots[i]];
     p->leave_group(r);  // after the append the tail block is private
@@ -850,12 +916,13 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
     if (r.n % B) r.group = p->new_group(1);
   }
   for (int i = 0; i < batch; ++i) p->touch(p->slots[slots[i]], true);
-  return run_append(p, ad, aa, x_dev, o_dev, S(stream));
+  return KV_OK;
 }
 
 kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream stream,
                      kv_state* out) {
   if (!p || !segs || !out || n < 1 || n > KV_MAX_SEGMENTS) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   const kv_model_cfg& c = p->cfg;
   const int B = c.block_size;
   std::vector<int32_t> sl(n);
@@ -912,7 +979,7 @@ kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream st
                               lineage_word(KV_LINEAGE_MERGE, (uint64_t)p->slots[sl[0]].sid, 0));
   {
     Timed t(p, KV_KERNEL_COMPOSE_META, s);
-    KV_HIP(launch_compose_meta(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks,
+    KV_LAUNCH(p, launch_compose_meta(p->dhdr, p->ring, p->rc, p->tables, p->max_blocks,
                                (int32_t)p->P, B, p->head, (int32_t)ncopy, ca, s));
   }
   p->head += ncopy;
@@ -926,7 +993,7 @@ kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream st
   }
   if (ncopy > 0) {
     Timed t(p, KV_KERNEL_COMPOSE_COPY, s);
-    KV_HIP(launch_compose_copy(p->geom(), c.dtype, ca, s));
+    KV_LAUNCH(p, launch_compose_copy(p->geom(), c.dtype, ca, s));
   }
   for (int i = 0; i < n; ++i) p->touch(p->slots[sl[i]], true);
   p->touch(r, false);
@@ -938,23 +1005,26 @@ static kv_status pack_impl(kv_pool* p, kv_state state, int64_t blk_begin, int64_
                            void* dst_dev, size_t dst_bytes, kv_pack_header* hdr_out,
                            kv_stream stream, bool checked) {
   if (!p || !dst_dev || !hdr_out) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   int32_t slot;
   KV_TRY(p->lookup(state, &slot));
   StateRec& r = p->slots[slot];
   if (!(0 <= blk_begin && blk_begin < blk_end && blk_end <= r.nblocks)) return KV_ERR_ARG;
   if ((uintptr_t)dst_dev & 15) return KV_ERR_ARG;
   const void* dst_view = nullptr;
-  KV_TRY(device_view(dst_dev, &dst_view));
+  bool dst_on_device = false;
+  KV_TRY(device_view(dst_dev, &dst_view, &dst_on_device));
   const kv_model_cfg& c = p->cfg;
   kv_pack_header h = make_header(p, r, blk_begin, blk_end);
   if (dst_bytes < h.payload_bytes) return KV_ERR_BUFSIZE;
+  if (dst_on_device) KV_TRY(device_span(p->device, dst_dev, h.payload_bytes));
   const int64_t nblk = h.n_blocks;
   const int32_t last_valid = (int32_t)(h.n_tokens - (nblk - 1) * c.block_size);
   const hipStream_t s = S(stream);
   if (checked) KV_TRY(csum_begin(p, s));
   {
     Timed t(p, KV_KERNEL_PACK, s);
-    KV_HIP(launch_pack(p->geom(), c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid,
+    KV_LAUNCH(p, launch_pack(p->geom(), c.dtype, p->trow(slot), blk_begin, (int32_t)nblk, last_valid,
                        const_cast<void*>(dst_view), checked ? p->csum : nullptr, 0, s));
   }
   if (checked) {
@@ -983,11 +1053,14 @@ kv_status kv_pack_checked(kv_pool* p, kv_state state, int64_t blk_begin, int64_t
 kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, size_t src_bytes,
                     kv_stream stream, kv_state* out) {
   if (!p || !hdr || !src_dev || !out) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   if ((uintptr_t)src_dev & 15) return KV_ERR_ARG;
   const void* src_view = nullptr;
-  KV_TRY(device_view(src_dev, &src_view));
+  bool src_on_device = false;
+  KV_TRY(device_view(src_dev, &src_view, &src_on_device));
   KV_TRY(check_header(p, hdr));
   if (src_bytes < hdr->payload_bytes) return KV_ERR_BUFSIZE;
+  if (src_on_device) KV_TRY(device_span(p->device, src_dev, hdr->payload_bytes));
   const hipStream_t s = S(stream);
   const bool checked = (hdr->flags & KV_PACK_CHECKSUM) != 0;
   int32_t slot;
@@ -995,7 +1068,7 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
   if (checked) KV_TRY(csum_begin(p, s));
   {
     Timed t(p, KV_KERNEL_UNPACK, s);
-    KV_HIP(launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot), (int32_t)hdr->n_blocks, src_view,
+    KV_LAUNCH(p, launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot), (int32_t)hdr->n_blocks, src_view,
                          checked ? p->csum : nullptr, 0, s));
   }
   if (checked) {
@@ -1014,6 +1087,7 @@ kv_status kv_unpack(kv_pool* p, const kv_pack_header* hdr, const void* src_dev, 
 
 kv_status kv_checkpoint_save(kv_pool* p, kv_state state, const char* path, kv_stream stream) {
   if (!p || !path) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   int32_t slot;
   KV_TRY(p->lookup(state, &slot));
   StateRec& r = p->slots[slot];
@@ -1036,7 +1110,7 @@ kv_status kv_checkpoint_save(kv_pool* p, kv_state state, const char* path, kv_st
                             : c.block_size;
     {
       Timed t(p, KV_KERNEL_PACK, s);
-      KV_HIP(launch_pack(p->geom(), c.dtype, p->trow(slot), b, (int32_t)k, last_valid,
+      KV_LAUNCH(p, launch_pack(p->geom(), c.dtype, p->trow(slot), b, (int32_t)k, last_valid,
                          const_cast<void*>(st.dev), p->csum,
                          (int64_t)(b * h.block_bytes / 16), s));
     }
@@ -1062,6 +1136,7 @@ kv_status kv_checkpoint_save(kv_pool* p, kv_state state, const char* path, kv_st
 
 kv_status kv_checkpoint_load(kv_pool* p, const char* path, kv_stream stream, kv_state* out) {
   if (!p || !path || !out) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   File f;
   f.f = std::fopen(path, "rb");
   if (!f.f) return KV_ERR_IO;
@@ -1089,7 +1164,7 @@ kv_status kv_checkpoint_load(kv_pool* p, const char* path, kv_stream stream, kv_
       return KV_ERR_IO;
     }
     Timed t(p, KV_KERNEL_UNPACK, s);
-    KV_HIP(launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot) + b, (int32_t)k, st.dev, p->csum,
+    KV_LAUNCH(p, launch_unpack(p->geom(), p->cfg.dtype, p->trow(slot) + b, (int32_t)k, st.dev, p->csum,
                          (int64_t)(b * h.block_bytes / 16), s));
   }
   uint64_t sum[2];
@@ -1105,6 +1180,7 @@ kv_status kv_checkpoint_load(kv_pool* p, const char* path, kv_stream stream, kv_
 
 kv_status kv_release(kv_pool* p, kv_state state, kv_stream stream) {
   if (!p) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   int32_t slot;
   KV_TRY(p->lookup(state, &slot));
   StateRec& r = p->slots[slot];
@@ -1127,6 +1203,7 @@ kv_status kv_pin(kv_pool* p, kv_state state, int32_t pinned) {
 kv_status kv_evict(kv_pool* p, int64_t max_allocated_blocks, double alpha, double beta,
                    double gamma, kv_stream stream, int32_t* n_evicted) {
   if (!p || !n_evicted || max_allocated_blocks < 0) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   *n_evicted = 0;
   const std::vector<int32_t> cand = eviction_candidates(p, alpha, beta, gamma);
   int32_t n = 0;
@@ -1144,6 +1221,7 @@ kv_status kv_evict_truncate(kv_pool* p, int64_t max_allocated_blocks, double alp
                             double gamma, kv_stream stream, int32_t* n_evicted,
                             int32_t* n_truncated) {
   if (!p || !n_evicted || !n_truncated || max_allocated_blocks < 0) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   *n_evicted = *n_truncated = 0;
   const std::vector<int32_t> cand = eviction_candidates(p, alpha, beta, gamma);
   int32_t n = 0;
@@ -1170,6 +1248,7 @@ kv_status kv_evict_truncate(kv_pool* p, int64_t max_allocated_blocks, double alp
 
 kv_status kv_sync(kv_pool* p, kv_stream stream) {
   if (!p) return KV_ERR_ARG;
+  if (p->failed) return KV_ERR_HIP;
   const hipStream_t s = S(stream);
   DevHeader h;
   KV_HIP(hipMemcpyAsync(&h, p->dhdr, sizeof(h), hipMemcpyDeviceToHost, s));
@@ -1195,6 +1274,18 @@ kv_status kv_state_info(kv_pool* p, kv_state state, int64_t* pos0, int64_t* n_to
   if (n_blocks) *n_blocks = r.nblocks;
   if (lineage) *lineage = r.lineage;
   if (state_id) *state_id = r.sid;
+  return KV_OK;
+}
+
+kv_status kv_state_usage(kv_pool* p, kv_state state, int64_t* reuse, int64_t* last_access,
+                         int32_t* pinned) {
+  if (!p) return KV_ERR_ARG;
+  int32_t slot;
+  KV_TRY(p->lookup(state, &slot));
+  const StateRec& r = p->slots[slot];
+  if (reuse) *reuse = r.reuse;
+  if (last_access) *last_access = r.last_access;
+  if (pinned) *pinned = r.pinned ? 1 : 0;
   return KV_OK;
 }
 

@@ -9,15 +9,19 @@
 // a chunk is one work unit.  The grouping is the same for every layer and KV
 // head, so it is computed once per call.
 //
-// k_decode_stream runs one wavefront per (unit, KV head, layer) with no
-// workgroup barriers: it streams the unit's K/V rows once, 32 keys at a time,
+// k_decode_stream runs one wavefront per (unit, query slice, KV head, layer)
+// with no workgroup barriers: it streams the unit's K/V rows once, 32 keys at a time,
 // through a ring of LDS stages filled by direct global->LDS copies, and scores
 // all of the group's query vectors (members x the G query heads of the KV
 // head) with MFMA in the transposed layout of the prefill kernel (query vector
 // in the MFMA column, softmax state lane-local, V^T operands by transposed LDS
 // reads).  Per (query vector, chunk) it writes a partial (running max m,
 // running sum l, unnormalised output o); k_decode_merge combines the chunks of
-// a query with the usual log-sum-exp rescaling.
+// a query with the usual log-sum-exp rescaling.  A unit's query vectors are
+// taken 64 at a time (two MFMA column tiles): a unit with more (e.g. 32
+// members x 4 query heads) is split into query slices, each a wavefront of
+// its own that streams the same keys; the slices of a unit are launched on
+// one XCD, so the later ones find the keys in its L2.
 #include <algorithm>
 
 #include "kv_dma.h"
@@ -149,14 +153,18 @@ __device__ inline void locate_unit(const int* __restrict__ n_units, int n_chunks
   }
 }
 
-// grid (slots, Hkv, lc), block 64.  Workgroup x takes units x, x + slots, ...
-// RT = query-vector tiles of 32 (a unit has at most 32 RT vectors); S = LDS
+// grid (slots x ns, Hkv, lc), block 64, ns = query slices per unit.  With
+// ns = 1, workgroup x takes units x, x + slots, ...; with ns > 1 (slots a
+// multiple of 8), x = (s / 8) * 8 ns + q * 8 + s % 8 takes slice q of units
+// s, s + slots, ..., so all slices of a unit have the same x mod 8 (XCD).
+// RT = query-vector tiles of 32 per slice (at most 32 RT vectors); S = LDS
 // stages (S - 1 in flight while one is consumed).
 template <int RT, int S>
 __global__ void __launch_bounds__(64)
 k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
                 const DecodeUnit* __restrict__ units, const int* __restrict__ n_units,
-                float* __restrict__ part, int n_chunks, int ck, int l0, float qk_scale_log2) {
+                float* __restrict__ part, int n_chunks, int ck, int l0, float qk_scale_log2,
+                int ns) {
   static_assert(S >= 2 && S <= 4, "stages");
   __shared__ __attribute__((aligned(16))) uint16_t smem[S * kStage];
   const int lane = threadIdx.x, hl = lane >> 5, col = lane & 31;
@@ -176,7 +184,11 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const uint32_t lds0 = lds_addr(smem);
   const int64_t kv_gap = (voff - koff) * 2;  // bytes from a K row to its V row
 
-  for (int u = blockIdx.x; u < total; u += gridDim.x) {
+  const int x = blockIdx.x;
+  const int slot = ns == 1 ? x : (x / (8 * ns)) * 8 + (x & 7);
+  const int qs = ns == 1 ? 0 : (x >> 3) % ns;
+  const int stride = gridDim.x / ns;
+  for (int u = slot; u < total; u += stride) {
     int c, gi;
     locate_unit(n_units, n_chunks, u, &c, &gi);
     c = __builtin_amdgcn_readfirstlane(c);
@@ -187,7 +199,9 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     const uint64_t mask = ((uint64_t)__builtin_amdgcn_readfirstlane(up->mask_hi) << 32) |
                           (uint32_t)__builtin_amdgcn_readfirstlane(up->mask_lo);
     const int R = __popcll(mask) * G;  // query vectors of the unit
-    const bool two = RT > 1 && R > 32;
+    const int q0 = qs * 32 * RT;       // this slice's first query vector
+    if (q0 >= R) continue;             // wave-uniform: a unit with fewer slices
+    const bool two = RT > 1 && R - q0 > 32;
     const int c0 = c * ck;
     // lane j: block id of the leader's entry j of the chunk (0 past the end)
     const int tbl = (lane << g.b_shift) < nk
@@ -200,7 +214,7 @@ k_decode_stream(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     int qrow[RT], qhead[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      const int r = rt * 32 + col;
+      const int r = q0 + rt * 32 + col;
       const bool ok = r < R;
       const int mi = ok ? r / G : 0;
       uint64_t mm = mask;
@@ -439,9 +453,9 @@ int decode_ck(const AppendDesc& a) { return a.batch == 1 ? kCK / 2 : kCK; }
 int decode_chunks(const AppendDesc& a) { return (a.max_keys + decode_ck(a) - 1) / decode_ck(a); }
 
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
-  const int G = g.Hq / g.Hkv;
-  // ck % B == 0 with B >= 16 a power of two: at most 64 block ids per chunk
-  return dtype == KV_DTYPE_BF16 && g.dh == kDh && a.T == 1 && a.batch * G <= 64 &&
+  // ck % B == 0 with B >= 16 a power of two: at most 64 block ids per chunk;
+  // any batch (query slices of 64 vectors cover batch x G)
+  return dtype == KV_DTYPE_BF16 && g.dh == kDh && a.T == 1 && a.batch <= KV_MAX_BATCH &&
          decode_ck(a) % g.B == 0 && g.B >= 16 && g.b_shift >= 0;
 }
 
@@ -484,18 +498,20 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
     k_decode_plan<<<nch, 64, dyn, s>>>(g, a, units, n_units, ck);
   }
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
-  const int slots = std::min(nch * a.batch, 2 * nch + a.batch);
-  dim3 grid(slots, g.Hkv, lc);
+  int slots = std::min(nch * a.batch, 2 * nch + a.batch);
+  const int ns = (a.batch * G + 63) / 64;  // query slices of 64 vectors
+  if (ns > 1) slots = (slots + 7) / 8 * 8;
+  dim3 grid(slots * ns, g.Hkv, lc);
   // one query tile: three 16 KiB stages per wave (two in flight), 3-4%
   // faster than two, while four are 9% slower; the number of bytes in flight
   // per CU, bounded by LDS, is what limits this stream.  Two query tiles (more
   // than 32 query vectors per unit): two stages, 15% faster than three.
   if (a.batch * G <= 32)
     k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
-                                              nch, ck, l0, sc);
+                                              nch, ck, l0, sc, 1);
   else
     k_decode_stream<2, 2><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
-                                              nch, ck, l0, sc);
+                                              nch, ck, l0, sc, ns);
   return hipGetLastError();
 }
 

@@ -17,19 +17,21 @@
 //            frequencies, position-major within a group, so that one load
 //            instruction reads consecutive positions), bf16 tile restaged
 //            through LDS so that the final Q / K / V stores are 16-byte,
-//            row-contiguous writes (k_qkv_mfma
-//            with register-staged LDS tiles when d is not a multiple of 64);
-//   M <= 16  k_qkv_decode_pst: each workgroup streams the weights of a group
-//            of (layer, head) tiles through per-wave LDS buffers without a
-//            break between tiles, token rows staged once per column chunk,
-//            one accumulator per tile, RoPE in registers;
-//            k_qkv_decode_dma when d is not a multiple of 256: weight
-//            streaming through per-wave LDS buffers
-//            filled by whole-cache-line copies, token rows staged in LDS
-//            (k_qkv_decode_lds, weights loaded straight into registers, when
-//            the buffers do not fit);
-//   M <= 32  k_qkv_decode / k_qkv_mfma<128, 32>: 128 channels (1 head) x 32
-//            tokens, fp32 tile in LDS for the rotation.
+//            row-contiguous writes (the fast path requires d % 64 == 0);
+//   M <= 16  k_qkv_decode_pst when d is a multiple of 256 and a column chunk
+//            of the token rows fits in 32 KiB of LDS (chunks halve while
+//            they are multiples of 512): each workgroup streams the weights
+//            of a group of (layer, head) tiles through per-wave LDS buffers
+//            without a break between tiles, token rows staged once per
+//            column chunk, one accumulator per tile, RoPE in registers;
+//            otherwise k_qkv_decode_lds (token rows staged in LDS, weights
+//            loaded straight into registers; d a multiple of 256, e.g. 2560
+//            with 13-16 rows), else k_qkv_decode<1> (token rows from global
+//            memory; d a multiple of 512 whose rows do not fit, e.g. 10752);
+//   M <= 32  k_qkv_decode<2> (d a multiple of 512) or k_qkv_mfma<128, 32>
+//            (any other d, and M <= 16 when d is not a multiple of 256):
+//            128 channels (1 head) x 32 tokens, fp32 tile in LDS for the
+//            rotation.
 // Q goes to the scratch buffer [lc][M][Hq * dh]; K and V rows go to
 // pool[table[slot][u / B]][l][K|V][kv head][u % B][:] with u = n_before + t.
 #include <atomic>
@@ -659,130 +661,19 @@ k_qkv_decode_lds(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __r
   }
 }
 
-// Decode-size projection with the weight stream copied into LDS by
-// non-temporal global->LDS copies.  The 16x16x32 MFMA operand layout asks for
-// 16 weight rows x 64 bytes per load instruction, which reads half cache
-// lines and streams ~12% slower (measured); here one copy instruction moves
-// 2 rows x 512 contiguous bytes instead.  Each wave copies and reads only its
-// own 16 rows, so the weight pipeline needs no workgroup barrier: batches of
-// kDmaKB k-steps (16 rows x 512 bytes), two per wave in LDS, the next one in
-// flight while the current one is multiplied.  Within a row's 512 bytes the
-// 16-byte chunk c sits in lane slot c ^ (row & 15), so that the 16 rows one
-// operand read touches fall in distinct bank groups.  Token rows are staged
-// in LDS as in k_qkv_decode_lds (column chunks of kc that fit beside the
-// weight buffers).  grid (N / 128, 1, lc), block 512, one workgroup per CU.
+// Weight stream of the decode-size projection: the 16x16x32 MFMA operand
+// layout asks for 16 weight rows x 64 bytes per load instruction, which reads
+// half cache lines and streams ~12% slower (measured), so each copy
+// instruction moves 2 rows x 512 contiguous bytes into LDS (non-temporal
+// global->LDS copies) instead.  Batches of kDmaKB k-steps (16 rows x 512
+// bytes), kDmaBuf per wave in LDS.  Each wave copies and reads only its own
+// 16 rows, so the stream needs no workgroup barrier; within a row's 512 bytes
+// the 16-byte chunk c sits in lane slot c ^ (row & 15), so that the 16 rows
+// one operand read touches fall in distinct bank groups.
 constexpr int kDmaKB = 8;                          // k-steps of 32 per batch
 constexpr int kDmaBuf = 2;                         // batches per wave in LDS
 constexpr int kDmaBatch = 16 * kDmaKB * 64;        // bytes of one batch (16 rows)
 constexpr int kDmaNI = kDmaBatch / 1024;           // copy instructions per batch
-constexpr size_t kDmaStatic =
-    (size_t)16 * (kDh + 4) * 4 + (size_t)kDecWaves * kDmaBuf * kDmaBatch;
-
-__global__ void __launch_bounds__(64 * kDecWaves)
-k_qkv_decode_dma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
-                 int64_t w_stride, AppendDesc a, uint16_t* __restrict__ qbuf, int l0, int kc) {
-  constexpr int FLD = kDh + 4;
-  constexpr int NT = 64 * kDecWaves;
-  constexpr int RPI = 1024 / (kDmaKB * 64);      // rows per copy instruction
-  constexpr int SPR = kDmaKB * 4;                // 16-byte slots per row and batch
-  __shared__ __attribute__((aligned(16))) float Cf[16 * FLD];
-  __shared__ __attribute__((aligned(16))) char wbuf[kDecWaves * kDmaBuf * kDmaBatch];
-  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][kc + 8]
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int lr = lane & 15, lg = lane >> 4;
-  const int n0 = blockIdx.x * kDh;
-  const int lc = blockIdx.z, l = l0 + lc;
-  const int M = a.batch * a.T, d = g.d, xld = kc + 8;
-  const char* wrows = (const char*)(w + (int64_t)l * w_stride + (int64_t)(n0 + wave * 16) * d);
-  const bool xok = lr < M;
-  const uint16_t* xr = xs + (xok ? lr : 0) * xld + lg * 8;
-
-  // copy j of a batch: rows RPI j + lane / SPR; lane slot s of a row holds
-  // the row's chunk s ^ (row & 15)
-  uint32_t voff[kDmaNI];
-#pragma unroll
-  for (int j = 0; j < kDmaNI; ++j) {
-    const int r = RPI * j + lane / SPR, sl = lane % SPR;
-    voff[j] = (uint32_t)r * d * 2 + (sl ^ (r & 15)) * 16;
-  }
-  const uint32_t lds_w = lds_addr(wbuf) + wave * kDmaBuf * kDmaBatch;
-  auto issue = [&](int b) {
-    const char* sb = wrows + (int64_t)b * kDmaKB * 64;
-    const uint32_t ld = lds_w + (b % kDmaBuf) * kDmaBatch;
-#pragma unroll
-    for (int j = 0; j < kDmaNI; ++j) lds_dma16_sv_nt(sb, voff[j], ld + j * 1024);
-  };
-  // this lane's weight row inside a batch buffer
-  const char* wrd = wbuf + wave * kDmaBuf * kDmaBatch + (lr / RPI) * 1024 + (lr % RPI) * SPR * 16;
-
-  const int nb = d / (kDmaKB * 32);
-  issue(0);
-  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int c8 = kc / 8;
-  int b = 0;
-  for (int kc0 = 0; kc0 < d; kc0 += kc) {
-    // token rows, columns [kc0, kc0 + kc), into LDS
-    if (kc0 > 0) __syncthreads();  // the previous chunk has been read
-    for (int i = tid; i < M * c8; i += NT) {
-      const int r = i / c8, c = i - r * c8;
-      *(uint4*)(xs + r * xld + c * 8) = *(const uint4*)(x + (int64_t)r * d + kc0 + c * 8);
-    }
-    __syncthreads();
-    const int b_end = (kc0 + kc) / (kDmaKB * 32);
-    for (; b < b_end; ++b) {
-      // the other buffer was read by the products of batch b - 1; a wave's
-      // copies complete in order, kDmaNI per batch
-      if (b + 1 < nb) {
-        issue(b + 1);
-        wait_vmcnt<kDmaNI>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      const char* wb = wrd + (b % kDmaBuf) * kDmaBatch;
-      const int kx = b * kDmaKB * 32 - kc0;
-#pragma unroll
-      for (int u = 0; u < kDmaKB; ++u) {
-        const int c = 4 * u + lg;
-        const uint4 fa = *(const uint4*)(wb + (c ^ lr) * 16);
-        const uint4 fb = xok ? *(const uint4*)(xr + kx + 32 * u) : make_uint4(0, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8v, fa),
-                                                      __builtin_bit_cast(bf16x8v, fb), acc, 0, 0,
-                                                      0);
-      }
-    }
-  }
-  // C[16 ch x 16 tok]: lane holds channels 4 (lane / 16) + e of token lane % 16
-  {
-    const int ch = wave * 16 + lg * 4;
-    *(float4*)(Cf + lr * FLD + ch) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-  }
-  __syncthreads();
-  const int half = kDh / 2;
-  const int hh = n0 / kDh;
-  for (int it = tid; it < 16 * (half / 4); it += NT) {
-    const int f4 = it % (half / 4), r = it / (half / 4);
-    if (r >= M) continue;
-    const float4 xv = *(const float4*)(Cf + r * FLD + f4 * 4);
-    const float4 yv = *(const float4*)(Cf + r * FLD + half + f4 * 4);
-    float4 xo = xv, yo = yv;
-    if (hh < g.Hq + g.Hkv) {
-      const int pos = row_info(a, r).pos;
-      const float4 cs = *(const float4*)(g.rope_cos + (int64_t)pos * half + f4 * 4);
-      const float4 sn = *(const float4*)(g.rope_sin + (int64_t)pos * half + f4 * 4);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float c = (&cs.x)[q], s = (&sn.x)[q];
-        (&xo.x)[q] = (&xv.x)[q] * c - (&yv.x)[q] * s;
-        (&yo.x)[q] = (&xv.x)[q] * s + (&yv.x)[q] * c;
-      }
-    }
-    uint16_t* dp = dest(g, a, qbuf, lc, l, M, r, hh, f4 * 4);
-    *(uint2*)dp = make_uint2(pack_bf16x2(xo.x, xo.y), pack_bf16x2(xo.z, xo.w));
-    *(uint2*)(dp + half) = make_uint2(pack_bf16x2(yo.x, yo.y), pack_bf16x2(yo.z, yo.w));
-  }
-}
-
 
 // Decode-size projection, workgroup-per-tile-group form: workgroup b takes
 // `tpw` consecutive (layer, head) tiles (tpw <= kPstTiles, chosen so that the
@@ -791,9 +682,8 @@ k_qkv_decode_dma(PoolGeom g, const uint16_t* __restrict__ x, const uint16_t* __r
 // whole row when it fits in kPstX bytes, with chunk c of row r at slot
 // c ^ (r & 15)); for each chunk the workgroup runs over its tiles, so a chunk
 // is staged once per workgroup rather than once per tile.  The weight stream
-// of k_qkv_decode_dma (2 rows x 512 bytes per non-temporal global->LDS copy,
-// two batches of 16 rows x 512 bytes per wave) runs on across tile and chunk
-// borders.  Wave w multiplies channels w * 8 .. w * 8 + 7 and their RoPE
+// (above: 2 rows x 512 bytes per non-temporal global->LDS copy, two batches
+// of 16 rows x 512 bytes per wave) runs on across tile and chunk borders.  Wave w multiplies channels w * 8 .. w * 8 + 7 and their RoPE
 // partners 64 + w * 8 .. 64 + w * 8 + 7, so that in the 16x16 output layout
 // the partners of lane l's values sit in lane l ^ 32: the rotation runs in
 // registers with factors loaded once, and each lane stores its 4 channels of
@@ -957,10 +847,6 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
   const size_t cf_bytes = 16 * (kDh + 4) * 4;
   while (kc % (2 * 32 * kDecU) == 0 && (size_t)M * (kc + 8) * 2 + cf_bytes > 80 * 1024) kc /= 2;
   const size_t x_lds = (size_t)M * (kc + 8) * 2;
-  // weight stream through LDS: token rows in column chunks of kd that fit
-  // beside the weight buffers
-  int kd = g.d;
-  while (kd % 512 == 0 && (size_t)M * (kd + 8) * 2 + kDmaStatic > 160 * 1024) kd /= 2;
   // token-row chunk of the tile-group kernel: the whole row, else halves, ...
   int kx = g.d;
   while ((size_t)M * kx * 2 > kPstX && kx % (2 * kDmaKB * 32) == 0) kx /= 2;
@@ -998,10 +884,6 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
     }
     k_qkv_decode_pst<<<(tiles + tpw - 1) / tpw, 64 * kDecWaves, (size_t)M * kx * 2, s>>>(
         g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0, lc, tpw, kx);
-  } else if (M <= 16 && kd % (kDmaKB * 32) == 0 && (size_t)M * (kd + 8) * 2 + kDmaStatic <= 160 * 1024) {
-    dim3 grid(N / kDh, 1, lc);
-    k_qkv_decode_dma<<<grid, 64 * kDecWaves, (size_t)M * (kd + 8) * 2, s>>>(
-        g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0, kd);
   } else if (M <= 16 && g.d % (32 * kDecU) == 0 && x_lds + cf_bytes <= 160 * 1024) {
     dim3 grid(N / kDh, 1, lc);
     k_qkv_decode_lds<<<grid, 64 * kDecWaves, x_lds, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
@@ -1018,14 +900,10 @@ hipError_t launch_qkv_mfma(const PoolGeom& g, const void* x, const void* w, int6
     dim3 grid(N / 128, 1, lc);
     k_qkv_mfma<128, 32, 4, 1><<<grid, kThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w,
                                                         w_stride, a, (uint16_t*)qbuf, l0);
-  } else if (g.d % kDlBK == 0) {
+  } else {  // qkv_mfma_ok: d % kDlBK == 0
     dim3 grid(N / 256, (M + 255) / 256, lc);
     k_qkv_dl<<<grid, kDlThreads, 0, s>>>(g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a,
                                           (uint16_t*)qbuf, l0);
-  } else {
-    dim3 grid(N / 256, (M + 255) / 256, lc);
-    k_qkv_mfma<256, 256, 2, 2><<<grid, kThreads, 0, s>>>(
-        g, (const uint16_t*)x, (const uint16_t*)w, w_stride, a, (uint16_t*)qbuf, l0);
   }
   return hipGetLastError();
 }

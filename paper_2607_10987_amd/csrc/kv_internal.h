@@ -60,9 +60,12 @@ struct AppendDesc {
 
 // Allocation requests, processed in order: if cow > 0, copy-on-write of the
 // entry `first - 1` (whose first `cow` slots hold valid tokens), then `count`
-// new entries starting at `first`.
+// new entries starting at `first`.  partial = valid slots of entry
+// `first - 1` when it is a partial tail block (0 otherwise): with cow == 0
+// the host holds that tail private, and the kernel checks that no other
+// table references it.
 struct AllocReq {
-  int32_t slot, first, count, cow;
+  int32_t slot, first, count, cow, partial;
 };
 struct AllocArgs {
   int32_t n_req;

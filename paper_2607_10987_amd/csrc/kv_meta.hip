@@ -11,7 +11,10 @@
 //    assigns ring slots, no atomics), states in the given order.
 // Each kernel is a single workgroup or touches disjoint ids, so results are
 // deterministic.  A mismatch with the host's expected counters sets the sticky
-// status KV_ERR_INTERNAL and the kernel does nothing.
+// status KV_ERR_INTERNAL and the kernel does nothing.  k_alloc also checks the
+// host's copy-on-write decisions against the refcounts in both directions (a
+// tail it copies must be shared, a partial tail it appends to in place must
+// not be) and sets the same status when they disagree.
 #include "kv_internal.h"
 
 namespace kvs {
@@ -51,6 +54,10 @@ k_alloc(DevHeader* hdr, int32_t* ring, int32_t* rc, int32_t* tables, int32_t max
         cow_pairs[r] = make_int2(old, nb);
       }
       pos += 1;
+    } else if (q.partial > 0 && threadIdx.x == 0 && rc[trow[q.first - 1]] != 1) {
+      // the host appends into a partial tail it holds alone; another table
+      // referencing it would see the append's tokens
+      hdr->status = KV_ERR_INTERNAL;
     }
     for (int i = threadIdx.x; i < q.count; i += blockDim.x) {
       const int32_t id = ring[(pos + i) % P];

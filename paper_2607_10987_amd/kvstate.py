@@ -101,6 +101,7 @@ _SIGS = {
     "kv_sync": (_I32, [_P, _P]),
     "kv_state_info": (_I32, [_P, _I64, _PI64, _PI64, _PI64, _PU64, _PI64]),
     "kv_pool_counts": (_I32, [_P, _PI64, _PI64, _PI64]),
+    "kv_state_usage": (_I32, [_P, _I64, _PI64, _PI64, _PI32]),
     "kv_read_block_table": (_I32, [_P, _I64, _PI32, _I64, _P]),
     "kv_read_allocator": (_I32, [_P, _PI32, _PI32, _PI64, _PI64, _P]),
     "kv_strerror": (ctypes.c_char_p, [_I32]),
@@ -161,6 +162,29 @@ def _check(st: int, where: str):
         raise KVError(st, where)
 
 
+# configuration of each live pool handle, for the tensor checks below
+_CFGS: dict = {}
+
+
+def _check_tensor(t, pool, min_elems: int, where: str):
+    """A torch tensor handed to a kernel must be a contiguous CUDA tensor of
+    the pool's dtype with at least ``min_elems`` elements; raise KVError
+    before the call otherwise.  Raw integer addresses are left to the
+    library's own checks."""
+    if t is None or isinstance(t, int):
+        return
+    cfg = _CFGS.get(pool)
+    if not getattr(t, "is_cuda", False) or not t.is_contiguous():
+        raise KVError(KV_ERR_ARG, where)
+    if cfg is not None:
+        import torch
+        want = torch.bfloat16 if cfg.dtype == KV_DTYPE_BF16 else torch.float32
+        if t.dtype != want:
+            raise KVError(KV_ERR_ARG, where)
+    if t.numel() < min_elems:
+        raise KVError(KV_ERR_BUFSIZE, where)
+
+
 def kv_strerror(status: int) -> str:
     return lib().kv_strerror(status).decode()
 
@@ -195,18 +219,33 @@ def kv_pool_create(cfg, n_blocks, pool, meta, scratch, scratch_bytes=None,
     _check(lib().kv_pool_create(ctypes.byref(cfg), n_blocks, _ptr(pool), _ptr(meta),
                                 _ptr(scratch), scratch_bytes, order, _stream(stream),
                                 ctypes.byref(out)), "kv_pool_create")
+    _CFGS[out.value] = kv_model_cfg.from_buffer_copy(cfg)
     return out.value
 
 
 def kv_pool_destroy(pool):
+    _CFGS.pop(pool, None)
     _check(lib().kv_pool_destroy(pool), "kv_pool_destroy")
 
 
+def _qkv_cols(c) -> int:
+    return (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim
+
+
 def kv_set_weights(pool, w, layer_stride_elems: int):
+    c = _CFGS.get(pool)
+    if c is not None:
+        per = _qkv_cols(c) * c.d_model
+        _check_tensor(w, pool, (c.n_layers - 1) * max(layer_stride_elems, 0) + per,
+                      "kv_set_weights")
     _check(lib().kv_set_weights(pool, _ptr(w), layer_stride_elems), "kv_set_weights")
 
 
 def kv_materialize(pool, x, T: int, pos0: int, o, stream=None) -> int:
+    c = _CFGS.get(pool)
+    if c is not None:
+        _check_tensor(x, pool, T * c.d_model, "kv_materialize x")
+        _check_tensor(o, pool, c.n_layers * T * c.n_q_heads * c.head_dim, "kv_materialize o")
     out = _I64()
     _check(lib().kv_materialize(pool, _ptr(x), T, pos0, _ptr(o), _stream(stream),
                                 ctypes.byref(out)), "kv_materialize")
@@ -269,6 +308,10 @@ def kv_unpack(pool, hdr: kv_pack_header, src, src_bytes=None, stream=None) -> in
 
 def kv_attend(pool, states, x, T: int, o, stream=None):
     n = len(states)
+    c = _CFGS.get(pool)
+    if c is not None:
+        _check_tensor(x, pool, n * T * c.d_model, "kv_attend x")
+        _check_tensor(o, pool, c.n_layers * n * T * c.n_q_heads * c.head_dim, "kv_attend o")
     arr = (ctypes.c_int64 * max(n, 1))(*[int(s) for s in states])
     _check(lib().kv_attend(pool, arr, n, _ptr(x), T, _ptr(o), _stream(stream)), "kv_attend")
 
@@ -309,6 +352,14 @@ def kv_state_info(pool, state: int):
                                ctypes.byref(lin), ctypes.byref(e)), "kv_state_info")
     return dict(pos0=a.value, n_tokens=b.value, n_blocks=c.value, lineage=lin.value,
                 state_id=e.value)
+
+
+def kv_state_usage(pool, state: int):
+    a, b = _I64(), _I64()
+    c = _I32()
+    _check(lib().kv_state_usage(pool, state, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)),
+           "kv_state_usage")
+    return dict(reuse=a.value, last_access=b.value, pinned=bool(c.value))
 
 
 def kv_pool_counts(pool):

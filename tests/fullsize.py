@@ -79,6 +79,10 @@ class MetaTwin:
             assert (info["pos0"], info["n_tokens"], info["n_blocks"], info["lineage"]) == \
                 self.orc.info(sid)
             assert kv.kv_read_block_table(self.h, h) == self.orc.table(sid), "block table"
+            st = self.orc.states[sid]
+            u = kv.kv_state_usage(self.h, h)
+            assert (u["reuse"], u["last_access"], u["pinned"]) == \
+                (st.reuse, st.last_access, st.pinned), ("eviction score terms", u)
 
     # ------------------------------------------------------------ device state
     def state_kv(self, h, layer):

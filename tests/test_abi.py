@@ -76,3 +76,59 @@ def test_scratch_bound_covers_decode_partials():
                 need = max(need, 32 * b * 32 * chunks * (4 + 128) * 4)
             got = kv.kv_scratch_bytes(c, 1, batch, keys)
             assert got >= need + q_bytes, (batch, keys, got, need)
+
+
+class _FakeCuda:
+    """Stands in for a CUDA tensor in the binding's argument checks (CPU)."""
+
+    def __init__(self, numel, dtype, contiguous=True):
+        self.is_cuda = True
+        self.dtype = dtype
+        self._n = numel
+        self._c = contiguous
+
+    def numel(self):
+        return self._n
+
+    def is_contiguous(self):
+        return self._c
+
+    def data_ptr(self):
+        raise AssertionError("the library was called with a bad tensor")
+
+
+def test_binding_rejects_bad_tensors_before_calling():
+    """x, o and w handed to kv_materialize / kv_attend / kv_set_weights must
+    be contiguous CUDA tensors of the pool's dtype, large enough for the
+    call; anything else raises KVError before the library is called."""
+    import pytest
+    import torch
+    c = kv.make_cfg(2, 64, 4, 2, 16, 4, "bf16", 128, 4)
+    handle = 0x5EED
+    kv._CFGS[handle] = c
+    bf = torch.bfloat16
+    try:
+        T, cols = 5, (4 + 2 * 2) * 16
+        for batch in (1, 3):
+            nx, no = batch * T * 64, 2 * batch * T * 4 * 16   # x [b][T][d], o [L][b][T][Hq dh]
+            cases = [
+                (torch.zeros(nx, dtype=bf), _FakeCuda(no, bf), kv.KV_ERR_ARG),       # CPU x
+                (_FakeCuda(nx, torch.float32), _FakeCuda(no, bf), kv.KV_ERR_ARG),   # dtype
+                (_FakeCuda(nx, bf, False), _FakeCuda(no, bf), kv.KV_ERR_ARG),       # strided
+                (_FakeCuda(nx - 1, bf), _FakeCuda(no, bf), kv.KV_ERR_BUFSIZE),
+                (_FakeCuda(nx, bf), _FakeCuda(no - 1, bf), kv.KV_ERR_BUFSIZE),
+                (_FakeCuda(nx, bf), torch.zeros(no, dtype=bf), kv.KV_ERR_ARG),      # CPU o
+            ]
+            for x, o, code in cases:
+                with pytest.raises(kv.KVError) as e:
+                    if batch == 1:
+                        kv.kv_materialize(handle, x, T, 0, o)
+                    else:
+                        kv.kv_attend(handle, [1, 2, 3], x, T, o)
+                assert e.value.status == code, (batch, code)
+        stride = 11 * cols * 64
+        with pytest.raises(kv.KVError) as e:
+            kv.kv_set_weights(handle, _FakeCuda(stride + cols * 64 - 1, bf), stride)
+        assert e.value.status == kv.KV_ERR_BUFSIZE
+    finally:
+        kv._CFGS.pop(handle, None)

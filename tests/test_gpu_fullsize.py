@@ -14,7 +14,9 @@ import torch
 
 import synth
 from fullsize import MetaTwin, close, close_rerotated, ref_kv, ref_rows, sample_rows, to64
+from oracle import rerotate
 from paper_2607_10987_amd import kvstate as kv
+from twin import close_one_rounding
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -98,9 +100,17 @@ def test_fork4_8b_full_size(gpu_available):
             kn, vn = ref_kv(mt, layer, xa, ctx + j * cont + np.arange(cont))
             comp_k.append(kn)
             comp_v.append(vn)
-            assert torch.equal(mt.state_kv(c, layer)[1][:, ctx + j * cont:ctx + (j + 1) * cont],
-                               vg[:, ctx:]), "composed values must be the source bytes"
+            kc_j, vc_j = (t[:, ctx + j * cont:ctx + (j + 1) * cont] for t in mt.state_kv(c, layer))
+            assert torch.equal(vc_j, vg[:, ctx:]), "composed values must be the source bytes"
+            # keys: the oracle's re-rotation of the agent's stored keys (one rounding)
+            if j == 0:
+                assert torch.equal(kc_j, kg[:, ctx:]), "unshifted keys must be copied"
+            else:
+                close_one_rounding(to64(kc_j), rerotate(to64(kg[:, ctx:]), j * cont, s.rope_base),
+                                   "bf16", f"re-rotated keys of agent {j}")
         kc, vc = mt.state_kv(c, layer)
+        assert torch.equal(kc[:, :ctx], kr) and torch.equal(vc[:, :ctx], vr), \
+            "the context's blocks are aliased"
         close_rerotated(to64(kc), np.concatenate(comp_k, axis=1), "bf16", "composed K")
         close(to64(vc), np.concatenate(comp_v, axis=1), "bf16", "composed V")
         ku, vu = mt.state_kv(u, layer)
@@ -242,6 +252,19 @@ def test_compose8_8b_full_size(gpu_available):
         tok = sample_rows(N, B, 1024, rng)
         close_rerotated(to64(kg[:, tok]), k_c[:, tok], "bf16", "composed K (sampled)")
         close(to64(vg[:, tok]), v_c[:, tok], "bf16", "composed V (sampled)")
+        # against the agents' own stored keys and values: values bit for bit
+        # (every token), keys one rounding from the oracle's re-rotation of
+        # the stored source keys (sampled tokens of every segment)
+        for j in range(A):
+            ks_j, vs_j = mt.state_kv(agents[j], layer)
+            kc_j, vc_j = kg[:, j * seg:(j + 1) * seg], vg[:, j * seg:(j + 1) * seg]
+            assert torch.equal(vc_j, vs_j), f"composed values of segment {j} must be the source bytes"
+            if j == 0:
+                assert torch.equal(kc_j, ks_j), "segment 0 is aliased"
+                continue
+            t = sample_rows(seg, B, 256, rng)
+            close_one_rounding(to64(kc_j[:, t]), rerotate(to64(ks_j[:, t]), j * seg, s.rope_base),
+                               "bf16", f"re-rotated keys of segment {j}, layer {layer}")
         k_t, v_t = ref_kv(mt, layer, np.concatenate([xa64, xd64]), N + np.arange(suf + ndec))
         kk = np.concatenate([k_c, k_t], axis=1)
         vv = np.concatenate([v_c, v_t], axis=1)

@@ -32,7 +32,7 @@ def test_tiny_workload(gpu_available):
         tw.attend([c], 1)
     n = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
     hdr, ohdr, buf, pay = tw.pack(c, 0, n)
-    u = tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    u = tw.unpack(hdr, ohdr, buf, pay, rerotated_from=c)
     tw.attend([u, a1], 3)
     tw.close()
 
@@ -114,7 +114,8 @@ def test_random_sequences_on_device(gpu_available, seed):
                 nb = kv.kv_state_info(tw.gpu.h, h)["n_blocks"]
                 b0 = int(rng.integers(0, nb))
                 hdr, ohdr, buf, pay = tw.pack(h, b0, nb)
-                handles.append(tw.unpack(hdr, ohdr, buf, pay, rerotated=h in tw.rerot))
+                handles.append(tw.unpack(hdr, ohdr, buf, pay,
+                                         rerotated_from=h if h in tw.rerot else None))
             elif op == 5:
                 tw.evict(int(rng.integers(0, 40)))
             elif op == 6:
@@ -143,7 +144,7 @@ def test_bf16_llama_shape_two_layers(gpu_available):
     c = tw.compose([(root, 0, 1000), (kids[0], 1000, 1100), (kids[1], 1000, 1100)])
     tw.attend([c], 1)
     hdr, ohdr, buf, pay = tw.pack(c, 2, 40)
-    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated_from=c)
     tw.close()
 
 
@@ -166,7 +167,7 @@ def test_bf16_70b_heads_two_layers(gpu_available):
     tw.attend([c], 1)
     nb = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
     hdr, ohdr, buf, pay = tw.pack(c, 0, nb)
-    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated_from=c)
     tw.close()
 
 
@@ -225,8 +226,8 @@ def test_pack_unpack_pinned_host_tier(gpu_available):
 
 def test_error_codes_on_device(gpu_available):
     tw = Twin(small_shape(B=2), n_blocks=4, max_pos=16, max_states=3, wl="err")
-    x = torch.zeros((9, 32), dtype=torch.float32, device="cuda")
-    o = torch.zeros((1, 9, 32), dtype=torch.float32, device="cuda")
+    x = torch.zeros((16, 32), dtype=torch.float32, device="cuda")
+    o = torch.zeros((1, 16, 32), dtype=torch.float32, device="cuda")
     with pytest.raises(kv.KVError) as e:
         kv.kv_materialize(tw.gpu.h, x, 9, 0, o)
     assert e.value.status == kv.KV_ERR_OOM
@@ -271,6 +272,41 @@ def test_error_codes_on_device(gpu_available):
     tw.close()
 
 
+def test_buffer_checks_before_any_launch(gpu_available):
+    """The C ABI checks every device buffer before it launches anything:
+    host memory and misaligned pointers are KV_ERR_ARG, an allocation that
+    ends before the bytes the call needs is KV_ERR_BUFSIZE.  Exercised
+    through kv_set_weights (which launches nothing) with raw addresses that
+    bypass the binding's own tensor checks, and through the binding."""
+    import ctypes
+    import os
+    shape = small_shape("bf16", B=16, dh=128, L=2, d=256, hq=4, hkv=2)
+    tw = Twin(shape, n_blocks=8, max_pos=64, wl="bufchk")
+    h = tw.gpu.h
+    per = shape.qkv_cols * shape.d_model
+    host = (ctypes.c_uint16 * (2 * per))()
+    hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
+    base, size = ctypes.c_void_p(), ctypes.c_size_t()
+    assert hip.hipMemGetAddressRange(ctypes.byref(base), ctypes.byref(size),
+                                     ctypes.c_void_p(tw.w_dev.data_ptr())) == 0
+    near_end = (base.value + size.value - 4096) & ~15
+    for ptr, code in ((ctypes.addressof(host), kv.KV_ERR_ARG),
+                      (tw.w_dev.data_ptr() + 2, kv.KV_ERR_ARG),
+                      (near_end, kv.KV_ERR_BUFSIZE)):
+        assert kv.lib().kv_set_weights(h, ptr, per) == code
+    # the binding refuses what the library would, before calling it
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_set_weights(h, tw.w_dev.float(), per)
+    assert e.value.status == kv.KV_ERR_ARG
+    with pytest.raises(kv.KVError) as e:
+        kv.kv_set_weights(h, tw.w_dev.reshape(-1)[:per], per)
+    assert e.value.status == kv.KV_ERR_BUFSIZE
+    # the weights set at construction are still in use: the pool works
+    s = tw.materialize(20)
+    tw.attend([s], 3)
+    tw.close()
+
+
 def test_bf16_fanout_decode_sixteen_agents(gpu_available):
     """16 agents x 4 query heads share a context: 64 query vectors per KV head in
     the shared chunks, private tails per agent, chunk boundaries crossed."""
@@ -293,7 +329,7 @@ def test_bf16_ragged_edges(gpu_available):
     kernel: a one-token state (decode-path kernels over a single key),
     prefills of 33 and 300 tokens (partial 256-row projection and 64-token
     attention tiles), decode batches of 3, 5 and 17 (17 agents x 4 query heads
-    is beyond the MFMA decode path: portable kernels at the real head shape,
+    = 68 query vectors per KV head: two query slices of the MFMA decode path,
     and 17 token rows for the projection), appends of 2 x 33 rows and of 70
     rows behind 301 cached tokens, a three-segment compose and a pack / unpack
     of the result."""
@@ -314,7 +350,7 @@ def test_bf16_ragged_edges(gpu_available):
     tw.attend([c], 1)
     nb = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
     hdr, ohdr, buf, pay = tw.pack(c, 0, nb)
-    tw.unpack(hdr, ohdr, buf, pay, rerotated=True)
+    tw.unpack(hdr, ohdr, buf, pay, rerotated_from=c)
     tw.close()
 
 

@@ -7,7 +7,14 @@ fed the same seeded inputs, and compares after each call:
 * block tables, refcounts, the free ring and its counters, state metadata:
   bit-exact;
 * attention outputs and pool K/V contents: max-abs and relative-L2 bounds
-  (bf16: 2e-2 / 5e-3; float32: 1e-4 / 1e-5).
+  (bf16: 2e-2 / 5e-3; float32: 1e-4 / 1e-5);
+* the eviction score terms of every live state (reuse count, last access,
+  pinned flag): exact;
+* keys that a composition re-rotated: against the oracle's re-rotation of the
+  device's own stored source keys, within half a unit in the last place of
+  the storage type plus float32 arithmetic noise (one rounding), and values
+  bit-exactly against the device's source values; later checks of such a
+  state compare those tokens bit-exactly with what the composition wrote.
 """
 from __future__ import annotations
 
@@ -15,7 +22,7 @@ import numpy as np
 import torch
 
 import synth
-from oracle import OraclePool
+from oracle import OraclePool, rerotate
 from oracle.pool import PoolShape
 from paper_2607_10987_amd import kvstate as kv
 
@@ -59,6 +66,31 @@ def close_rerotated(got, want, dtype, what=""):
     return float(err.max()), rel
 
 
+def half_ulp(x, dtype):
+    """Half a unit in the last place of |x| in the storage type."""
+    mant = 8 if dtype == "bf16" else 24          # significand bits incl. the implicit one
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -100)))
+    return np.ldexp(1.0, (e - mant).astype(np.int64))
+
+
+def close_one_rounding(got, want, dtype, what=""):
+    """got = the storage rounding of a float32 evaluation of want: each element
+    within half an ulp (taken at |want| + noise) plus the float32 noise of a
+    rotation, 2^-21 times the norm of the element's rotation pair."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    half = want.shape[-1] // 2
+    pn = np.sqrt(want[..., :half] ** 2 + want[..., half:] ** 2)
+    noise = 2.0 ** -21 * np.concatenate([pn, pn], axis=-1)
+    bound = half_ulp(np.abs(want) + noise, dtype) + noise
+    err = np.abs(got - want)
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {int(bad.sum())} of {bad.size} elements beyond one "
+                           f"rounding, worst excess {float((err - bound).max()):.3e}")
+    return float(err.max())
+
+
 def to_np(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
@@ -66,7 +98,7 @@ def to_np(t: torch.Tensor) -> np.ndarray:
 class Twin:
     def __init__(self, shape: synth.ModelShape, n_blocks: int, max_pos: int, max_states: int = 32,
                  seed: int = 0, wl: str = "twin", order=None, scratch_tokens: int = 4096,
-                 check_kv: bool = True, model_id: int = 7):
+                 check_kv: bool = True, model_id: int = 7, scratch_bytes: int = None):
         self.s = shape
         self.seed = seed
         self.wl = wl
@@ -83,7 +115,8 @@ class Twin:
         self.cfg = kv.make_cfg(L, d, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
                                shape.block_size, self.dt, max_pos, max_states,
                                shape.rope_base, model_id)
-        scratch = kv.kv_scratch_bytes(self.cfg, scratch_tokens, 8, max_pos)
+        scratch = kv.kv_scratch_bytes(self.cfg, scratch_tokens, 8, max_pos) \
+            if scratch_bytes is None else scratch_bytes
         self.gpu = kv.Pool(self.cfg, n_blocks, scratch, init_free_order=order)
         self.gpu.set_weights(self.w_dev, cols * d)
         pshape = PoolShape(L, d, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
@@ -91,7 +124,7 @@ class Twin:
                            model_id)
         self.orc = OraclePool(pshape, n_blocks, init_free_order=order, weights=w64)
         self.sid = {}        # gpu handle -> oracle state id
-        self.rerot = set()   # handles holding keys re-rotated by compose
+        self.rerot = {}      # handle -> device K [L][Hkv, n, dh] a composition wrote
         self.calls = 0
 
     # -------------------------------------------------------------- inputs
@@ -123,11 +156,16 @@ class Twin:
             assert (info["pos0"], info["n_tokens"], info["n_blocks"], info["lineage"]) == \
                 self.orc.info(sid), ("state info", info, self.orc.info(sid))
             assert kv.kv_read_block_table(self.gpu.h, h) == self.orc.table(sid), "block table"
+            u = kv.kv_state_usage(self.gpu.h, h)
+            assert (u["reuse"], u["last_access"], u["pinned"]) == \
+                (st.reuse, st.last_access, st.pinned), ("eviction score terms", u)
         c = kv.kv_pool_counts(self.gpu.h)
         assert c["free_blocks"] == self.orc.free_count()
         assert c["clock"] == self.orc.clock
 
-    def gpu_state_kv(self, h, layer):
+    def gpu_state_kv_raw(self, h, layer):
+        """Device K and V of a state's valid tokens: two [Hkv, n, dh] tensors
+        of the storage type."""
         table = kv.kv_read_block_table(self.gpu.h, h)
         n = kv.kv_state_info(self.gpu.h, h)["n_tokens"]
         blocks = self.gpu.blocks_view()[table, layer]         # [nb, 2, Hkv, B, dh]
@@ -135,8 +173,11 @@ class Twin:
         # valid slots only: the slots past the last token are unspecified and
         # may hold any bit pattern (signalling NaNs included)
         x = blocks.permute(1, 2, 0, 3, 4).reshape(2, hkv, nb * B, dh)[:, :, :n]
-        x = to_np(x)
         return x[0], x[1]
+
+    def gpu_state_kv(self, h, layer):
+        k, v = self.gpu_state_kv_raw(h, layer)
+        return to_np(k), to_np(v)
 
     def check_state_kv(self, h):
         sid = self.sid[h]
@@ -144,10 +185,43 @@ class Twin:
             k, v = self.gpu_state_kv(h, layer)
             ko, vo = self.orc.state_kv(sid, layer)
             if h in self.rerot:
-                close_rerotated(k, ko, self.dt, f"re-rotated K layer {layer}")
+                m = min(self.rerot[h][layer].shape[1], k.shape[1])
+                kr, _ = self.gpu_state_kv_raw(h, layer)
+                assert torch.equal(kr[:, :m], self.rerot[h][layer][:, :m]), \
+                    f"composed keys changed, layer {layer}"
+                close(k[:, m:], ko[:, m:], self.dt, f"K after the composition, layer {layer}")
+                close_rerotated(k[:, :m], ko[:, :m], self.dt, f"re-rotated K layer {layer}")
             else:
                 close(k, ko, self.dt, f"K layer {layer}")
             close(v, vo, self.dt, f"V layer {layer}")
+
+    def check_compose_kv(self, h, segs):
+        """A composition against the device's own source state: per segment,
+        keys = the oracle's re-rotation of the stored source keys by the
+        segment's shift (one rounding), values = the source values bit for
+        bit.  Records the composed keys for later checks of the state."""
+        info = {a: kv.kv_state_info(self.gpu.h, a) for a, _, _ in segs}
+        p_dst = info[segs[0][0]]["pos0"] + segs[0][1]
+        snap = []
+        for layer in range(self.s.n_layers):
+            kd, vd = self.gpu_state_kv_raw(h, layer)
+            cum = 0
+            for a, b, e in segs:
+                ks, vs = self.gpu_state_kv_raw(a, layer)
+                delta = p_dst + cum - (info[a]["pos0"] + b)
+                n = e - b
+                assert torch.equal(vd[:, cum:cum + n], vs[:, b:e]), \
+                    f"composed V differs from its source, layer {layer}"
+                if delta == 0:
+                    assert torch.equal(kd[:, cum:cum + n], ks[:, b:e]), \
+                        f"unshifted composed K differs from its source, layer {layer}"
+                else:
+                    want = rerotate(to_np(ks[:, b:e]), delta, self.s.rope_base)
+                    close_one_rounding(to_np(kd[:, cum:cum + n]), want, self.dt,
+                                       f"re-rotated K (shift {delta}), layer {layer}")
+                cum += n
+            snap.append(kd.clone())
+        self.rerot[h] = snap
 
     def _after(self, *handles):
         self.calls += 1
@@ -176,7 +250,7 @@ class Twin:
         for a, b in zip(kids, okids):
             self.sid[a] = b
             if h in self.rerot:
-                self.rerot.add(a)
+                self.rerot[a] = self.rerot[h]
         self._after()
         return kids
 
@@ -197,7 +271,8 @@ class Twin:
         h = kv.kv_compose(self.gpu.h, segs)
         sid = self.orc.compose([(self.sid[a], b, c) for a, b, c in segs])
         self.sid[h] = sid
-        self.rerot.add(h)   # shifted segments carry re-rotated keys
+        torch.cuda.synchronize()
+        self.check_compose_kv(h, segs)   # shifted segments carry re-rotated keys
         self._after(h)
         return h
 
@@ -221,13 +296,16 @@ class Twin:
         self._after()
         return hdr, ohdr, buf, payload
 
-    def unpack(self, hdr, ohdr, buf, payload64, rerotated=False):
-        """Device unpacks its buffer, the oracle its own payload."""
+    def unpack(self, hdr, ohdr, buf, payload64, rerotated_from=None):
+        """Device unpacks its buffer, the oracle its own payload.
+        rerotated_from: the composed state the buffer was packed from (its
+        recorded keys then apply to the unpacked state)."""
         h = kv.kv_unpack(self.gpu.h, hdr, buf)
         sid = self.orc.unpack(ohdr, payload64)
         self.sid[h] = sid
-        if rerotated:
-            self.rerot.add(h)
+        if rerotated_from is not None:
+            lo = hdr.blk_begin * self.s.block_size
+            self.rerot[h] = [k[:, lo:lo + hdr.n_tokens] for k in self.rerot[rerotated_from]]
         self._after(h)
         return h
 
