@@ -336,16 +336,16 @@ kv_status run_release(kv_pool* p, const std::vector<int32_t>& cand, int64_t max_
   return KV_OK;
 }
 
-// Per-call launch description of an append (materialize or attend).
-AppendDesc make_desc(const kv_pool* p, const std::vector<int32_t>& slots,
-                     const std::vector<int64_t>& n_before, const std::vector<int64_t>& pos0,
-                     int64_t T) {
+// Per-call launch description of an append (materialize or attend) of T
+// tokens to `batch` states (catalog slots, tokens cached, position of token 0).
+AppendDesc make_desc(int32_t batch, const int32_t* slots, const int64_t* n_before,
+                     const int64_t* pos0, int64_t T) {
   AppendDesc ad;
   std::memset(&ad, 0, sizeof(ad));
-  ad.batch = (int32_t)slots.size();
+  ad.batch = batch;
   ad.T = (int32_t)T;
   int32_t max_keys = 0;
-  for (size_t i = 0; i < slots.size(); ++i) {
+  for (int32_t i = 0; i < batch; ++i) {
     ad.seq[i].slot = slots[i];
     ad.seq[i].n_before = (int32_t)n_before[i];
     ad.seq[i].pos0 = (int32_t)pos0[i];
@@ -355,23 +355,35 @@ AppendDesc make_desc(const kv_pool* p, const std::vector<int32_t>& slots,
   return ad;
 }
 
-// Layers per group that fit in the scratch area (0: not even one layer).
-int layers_per_group(const kv_pool* p, const AppendDesc& ad, size_t* q_layer, size_t* extra) {
+// Layout of an append's scratch area: the query rows of each layer of a group
+// ([lc][M][Hq dh]), then the attention's per-layer area (split-key partials),
+// then its per-call area (the decode work plan).
+struct ScratchPlan {
+  size_t q_layer, part_layer, fixed;
+  int lc_max;  // layers per group; 0 when not even one layer fits
+};
+
+ScratchPlan plan_scratch(const kv_pool* p, const AppendDesc& ad, size_t scratch_bytes) {
   const kv_model_cfg& c = p->cfg;
   const int64_t M = (int64_t)ad.batch * ad.T;
-  *q_layer = align256((size_t)M * c.n_q_heads * c.head_dim * elt_bytes(c));
-  *extra = align256(fast_scratch_bytes(p->geom(), c.dtype, ad));
-  if (p->scratch_bytes < *q_layer + *extra) return 0;
-  return (int)std::min<size_t>(c.n_layers, (p->scratch_bytes - *extra) / *q_layer);
+  ScratchPlan sp;
+  sp.q_layer = align256((size_t)M * c.n_q_heads * c.head_dim * elt_bytes(c));
+  fast_scratch_need(p->geom(), c.dtype, ad, &sp.part_layer, &sp.fixed);
+  const size_t per = sp.q_layer + sp.part_layer;
+  sp.lc_max = scratch_bytes < sp.fixed + per
+                  ? 0
+                  : (int)std::min<size_t>(c.n_layers, (scratch_bytes - sp.fixed) / per);
+  return sp;
 }
 
 // Shared path of materialize and attend: allocation (with copy-on-write),
-// projection + RoPE + paged store, and attention, layer group by layer group.
+// projection + RoPE + paged store, and attention, layer group by layer group,
+// with `scratch` (scratch_bytes) as the work area.
 kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, const void* x,
-                     void* o, hipStream_t s) {
+                     void* o, hipStream_t s, char* scratch, size_t scratch_bytes) {
   const kv_model_cfg& c = p->cfg;
-  size_t q_layer, extra;
-  const int lc_max = layers_per_group(p, ad, &q_layer, &extra);
+  const ScratchPlan sp = plan_scratch(p, ad, scratch_bytes);
+  const int lc_max = sp.lc_max;
   if (lc_max < 1) return KV_ERR_BUFSIZE;
   KV_TRY(run_alloc(p, aa, s));
   const PoolGeom g = p->geom();
@@ -381,23 +393,26 @@ kv_status run_append(kv_pool* p, const AppendDesc& ad, const AllocArgs& aa, cons
     Timed t(p, KV_KERNEL_COW, s);
     KV_LAUNCH(p, launch_cow(g, c.dtype, p->cow, aa, s));
   }
-  void* part = p->scratch + q_layer * lc_max;
+  char* part = scratch + sp.q_layer * lc_max;
+  char* plan = part + sp.part_layer * lc_max;
   for (int l0 = 0; l0 < c.n_layers; l0 += lc_max) {
     const int lc = std::min(lc_max, c.n_layers - l0);
     bool done = false;
     {
       Timed t(p, ad.T == 1 ? KV_KERNEL_QKV_DECODE : KV_KERNEL_QKV, s);
-      KV_LAUNCH(p, launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s,
-                             &done));
+      KV_LAUNCH(p, launch_qkv_fast(g, c.dtype, x, p->w, p->w_stride, ad, scratch, l0, lc, s,
+                                   &done));
       if (!done)
-        KV_LAUNCH(p, launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, p->scratch, l0, lc, s));
+        KV_LAUNCH(p, launch_qkv_generic(g, c.dtype, x, p->w, p->w_stride, ad, scratch, l0, lc,
+                                        s));
     }
     done = false;
     bool merge = false;
     {
       Timed t(p, ad.T == 1 ? KV_KERNEL_ATTN_DECODE : KV_KERNEL_ATTN, s);
-      KV_LAUNCH(p, launch_attn_fast(g, c.dtype, p->scratch, ad, o, part, l0, lc, s, &done, &merge));
-      if (!done) KV_LAUNCH(p, launch_attn_generic(g, c.dtype, p->scratch, ad, o, l0, lc, s));
+      KV_LAUNCH(p, launch_attn_fast(g, c.dtype, scratch, ad, o, part, plan, l0, lc, s, &done,
+                                    &merge));
+      if (!done) KV_LAUNCH(p, launch_attn_generic(g, c.dtype, scratch, ad, o, l0, lc, s));
     }
     if (merge) {
       Timed t(p, KV_KERNEL_MERGE, s);
@@ -729,6 +744,9 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   p->head = 0;
   p->tail = n_blocks;
   p->slots.resize(cfg->max_states);
+  // at most one tail group per live state: no reallocation after creation
+  p->holders.reserve(cfg->max_states);
+  p->free_groups.reserve(cfg->max_states);
 
   // RoPE table: angle p * theta_i with theta_i = base^(-2i/dh), in double.
   const int half = cfg->head_dim / 2;
@@ -805,16 +823,16 @@ kv_status kv_materialize(kv_pool* p, const void* x_dev, int64_t T, int64_t pos0,
   if (slot < 0) return KV_ERR_CAPACITY;
   const int64_t nb = ceil_div(T, c.block_size);
   if (nb > p->free_blocks()) return KV_ERR_OOM;
-  const AppendDesc ad = make_desc(p, {slot}, {0}, {pos0}, T);
-  size_t ql, ex;
-  if (layers_per_group(p, ad, &ql, &ex) < 1) return KV_ERR_BUFSIZE;
+  const int64_t zero = 0;
+  const AppendDesc ad = make_desc(1, &slot, &zero, &pos0, T);
+  if (plan_scratch(p, ad, p->scratch_bytes).lc_max < 1) return KV_ERR_BUFSIZE;
   AllocArgs aa;
   std::memset(&aa, 0, sizeof(aa));
   aa.n_req = 1;
   aa.req[0].slot = slot;
   aa.req[0].count = (int32_t)nb;
   // the catalog changes only once every launch of the call is enqueued
-  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
+  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream), p->scratch, p->scratch_bytes));
   StateRec& r = p->open_state(slot, pos0, T, nb,
                               lineage_word(KV_LINEAGE_MATERIALIZE, kNoParent, 0));
   if (T % c.block_size) r.group = p->new_group(1);
@@ -857,8 +875,13 @@ kv_status kv_fork(kv_pool* p, kv_state parent, int32_t k, kv_state* children, kv
   return KV_OK;
 }
 
-kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const void* x_dev,
-                    int64_t T, void* o_dev, kv_stream stream) {
+}  // extern "C"
+
+// KV-Resume over a batch with `scratch` as the work area.  Uses no heap
+// memory on the host (fixed arrays of KV_MAX_BATCH) and none on the device.
+static kv_status attend_impl(kv_pool* p, const kv_state* states, int32_t batch,
+                             const void* x_dev, int64_t T, void* o_dev, kv_stream stream,
+                             char* scratch, size_t scratch_bytes) {
   if (!p || !states || !x_dev || !o_dev || batch < 1 || batch > KV_MAX_BATCH || T <= 0)
     return KV_ERR_ARG;
   if (p->failed) return KV_ERR_HIP;
@@ -868,27 +891,27 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
       if (states[i] == states[j]) return KV_ERR_ARG;
   const kv_model_cfg& c = p->cfg;
   const int B = c.block_size;
-  std::vector<int32_t> slots(batch);
+  int32_t slots[KV_MAX_BATCH];
   for (int i = 0; i < batch; ++i) KV_TRY(p->lookup(states[i], &slots[i]));
   AllocArgs aa;
   std::memset(&aa, 0, sizeof(aa));
   aa.n_req = batch;
-  std::vector<int64_t> nbef(batch), pos0(batch);
+  int64_t nbef[KV_MAX_BATCH], pos0[KV_MAX_BATCH];
   int64_t need = 0;
-  // holders of each tail group as the batch is processed in order: a member
-  // that copies a shared tail leaves its group before the next member looks
-  std::vector<std::pair<int32_t, int32_t>> left;
+  // tail groups left by earlier members of the batch: a member that copies a
+  // shared tail leaves its group before the next member looks
+  int32_t left[KV_MAX_BATCH];
+  int n_left = 0;
   auto holders_now = [&](int32_t g) {
     int32_t h = p->holders[g];
-    for (const auto& e : left)
-      if (e.first == g) h -= e.second;
+    for (int i = 0; i < n_left; ++i) h -= left[i] == g;
     return h;
   };
   for (int i = 0; i < batch; ++i) {
     const StateRec& r = p->slots[slots[i]];
     if (r.pos0 + r.n + T > c.max_pos) return KV_ERR_CAPACITY;
     const bool shared_tail = (r.n % B) && r.group >= 0 && holders_now(r.group) > 1;
-    if (shared_tail) left.push_back({r.group, 1});
+    if (shared_tail) left[n_left++] = r.group;
     aa.req[i].slot = slots[i];
     aa.req[i].cow = shared_tail ? (int32_t)(r.n % B) : 0;
     aa.req[i].partial = (int32_t)(r.n % B);
@@ -899,15 +922,14 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
     pos0[i] = r.pos0;
   }
   if (need > p->free_blocks()) return KV_ERR_OOM;
-  const AppendDesc ad = make_desc(p, slots, nbef, pos0, T);
-  size_t ql, ex;
-  if (layers_per_group(p, ad, &ql, &ex) < 1) return KV_ERR_BUFSIZE;
+  const AppendDesc ad = make_desc(batch, slots, nbef, pos0, T);
+  if (plan_scratch(p, ad, scratch_bytes).lc_max < 1) return KV_ERR_BUFSIZE;
   const size_t elt = elt_bytes(c);
   KV_TRY(device_span(p->device, x_dev, (size_t)batch * T * c.d_model * elt));
   KV_TRY(device_span(p->device, o_dev,
                      (size_t)c.n_layers * batch * T * c.n_q_heads * c.head_dim * elt));
   // the catalog changes only once every launch of the call is enqueued
-  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream)));
+  KV_TRY(run_append(p, ad, aa, x_dev, o_dev, S(stream), scratch, scratch_bytes));
   for (int i = 0; i < batch; ++i) {
     StateRec& r = p->slots[slots[i]];
     p->leave_group(r);  // after the append the tail block is private
@@ -918,6 +940,15 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
   for (int i = 0; i < batch; ++i) p->touch(p->slots[slots[i]], true);
   return KV_OK;
 }
+
+extern "C" {
+
+kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const void* x_dev,
+                    int64_t T, void* o_dev, kv_stream stream) {
+  return attend_impl(p, states, batch, x_dev, T, o_dev, stream, p ? p->scratch : nullptr,
+                     p ? p->scratch_bytes : 0);
+}
+
 
 kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream stream,
                      kv_state* out) {

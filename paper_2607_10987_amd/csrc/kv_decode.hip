@@ -460,16 +460,19 @@ bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
 }
 
 namespace {
-size_t part_bytes(const PoolGeom& g, const AppendDesc& a) {
-  return ((size_t)g.L * a.batch * g.Hq * decode_chunks(a) * kPart * sizeof(float) + 255) & ~size_t(255);
-}
 size_t unit_bytes(const AppendDesc& a) {
   return ((size_t)decode_chunks(a) * a.batch * sizeof(DecodeUnit) + 255) & ~size_t(255);
 }
 }  // namespace
 
-size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a) {
-  return part_bytes(g, a) + unit_bytes(a) + (((size_t)decode_chunks(a) * sizeof(int) + 255) & ~size_t(255));
+// Split-key partials of one layer: [batch][Hq][chunks][kPart] floats.
+size_t decode_part_layer_bytes(const PoolGeom& g, const AppendDesc& a) {
+  return ((size_t)a.batch * g.Hq * decode_chunks(a) * kPart * sizeof(float) + 255) & ~size_t(255);
+}
+
+// The work plan: units [chunks][batch], then the unit count of each chunk.
+size_t decode_plan_bytes(const AppendDesc& a) {
+  return unit_bytes(a) + (((size_t)decode_chunks(a) * sizeof(int) + 255) & ~size_t(255));
 }
 
 size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_keys) {
@@ -486,13 +489,13 @@ size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_ke
 }
 
 hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
-                              void* scratch, int lc, int l0, hipStream_t s) {
+                              void* part_area, void* plan, int lc, int l0, hipStream_t s) {
   const int G = g.Hq / g.Hkv;
   const int nch = decode_chunks(a);
   const int ck = decode_ck(a);
-  float* part = (float*)scratch;
-  DecodeUnit* units = (DecodeUnit*)((char*)scratch + part_bytes(g, a));
-  int* n_units = (int*)((char*)units + unit_bytes(a));
+  float* part = (float*)part_area;
+  DecodeUnit* units = (DecodeUnit*)plan;
+  int* n_units = (int*)((char*)plan + unit_bytes(a));
   if (l0 == 0) {  // the grouping holds for every layer group of the call
     const size_t dyn = (size_t)a.batch * (ck / g.B) * sizeof(int);
     k_decode_plan<<<nch, 64, dyn, s>>>(g, a, units, n_units, ck);

@@ -5,15 +5,19 @@ namespace kvs {
 
 int decode_chunks(const AppendDesc& a);
 bool decode_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a);
-size_t decode_part_bytes(const PoolGeom& g, const AppendDesc& a);
+size_t decode_part_layer_bytes(const PoolGeom& g, const AppendDesc& a);
+size_t decode_plan_bytes(const AppendDesc& a);
 size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_keys);
 hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendDesc& a,
-                              void* part, int lc, int l0, hipStream_t s);
+                              void* part, void* plan, int lc, int l0, hipStream_t s);
 hipError_t launch_decode_merge(const PoolGeom& g, const AppendDesc& a, void* o, const void* part,
                                int l0, int lc, hipStream_t s);
 
-size_t fast_scratch_bytes(const PoolGeom& g, int dtype, const AppendDesc& a) {
-  return decode_mfma_ok(g, dtype, a) ? decode_part_bytes(g, a) : 0;
+void fast_scratch_need(const PoolGeom& g, int dtype, const AppendDesc& a, size_t* per_layer,
+                       size_t* fixed) {
+  const bool dec = decode_mfma_ok(g, dtype, a);
+  *per_layer = dec ? decode_part_layer_bytes(g, a) : 0;
+  *fixed = dec ? decode_plan_bytes(a) : 0;
 }
 
 size_t fast_scratch_bound(const kv_model_cfg& c, int64_t, int32_t batch, int64_t max_keys) {
@@ -39,14 +43,14 @@ hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const Append
                                int l0, int lc, hipStream_t s);
 
 hipError_t launch_attn_fast(const PoolGeom& g, int dtype, const void* qbuf, const AppendDesc& a,
-                            void* o, void* part, int l0, int lc, hipStream_t s, bool* done,
-                            bool* merge) {
+                            void* o, void* part, void* plan, int l0, int lc, hipStream_t s,
+                            bool* done, bool* merge) {
   *done = false;
   *merge = false;
   if (decode_mfma_ok(g, dtype, a)) {
     *done = true;
     *merge = true;
-    return launch_decode_attn(g, qbuf, a, part, lc, l0, s);
+    return launch_decode_attn(g, qbuf, a, part, plan, lc, l0, s);
   }
   if (!attn_mfma_ok(g, dtype, a)) return hipSuccess;
   *done = true;

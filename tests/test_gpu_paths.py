@@ -104,18 +104,16 @@ def test_layer_groups_prefill_and_append(gpu_available, per_group):
 def test_layer_groups_batched_decode(gpu_available, per_group):
     """A 2100-token context (a seeded payload unpacked into the pool) forked
     to 16 agents; batch-16 decode steps with a scratch area that holds the
-    split-key partials of all layers but the query rows of only `per_group`
-    of the 4 layers, so the work plan computed for the first group is reused
+    query rows and split-key partials of only `per_group` of the 4 layers
+    (plus the work plan), so the plan computed for the first group is reused
     by the others."""
     shape = shape8b(L=4)
     A, n_ctx = 16, 2100
-    cfg = kv.make_cfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
-                      shape.head_dim, shape.block_size, "bf16", 2304, A + 4)
+    chunks = -(-(n_ctx + 3) // 1024)          # keys per decode call <= n_ctx + 3
     q_layer = align256(A * shape.n_q_heads * shape.head_dim * 2)
-    # an upper bound of the partials and plan of a batch-16 decode over <= n_ctx + 4 keys
-    extra = kv.kv_scratch_bytes(cfg, A, A, n_ctx + 4) - \
-        align256(shape.n_layers * A * shape.n_q_heads * shape.head_dim * 2)
-    scratch = extra + per_group * q_layer + q_layer // 2
+    part_layer = align256(A * shape.n_q_heads * chunks * (shape.head_dim + 4) * 4)
+    plan = align256(chunks * A * 16) + align256(chunks * 4)
+    scratch = plan + per_group * (q_layer + part_layer) + q_layer // 2
     tw = Twin(shape, n_blocks=200, max_pos=2304, max_states=A + 4, wl="lgdec",
               scratch_bytes=scratch)
     nb = -(-n_ctx // shape.block_size)
