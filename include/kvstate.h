@@ -78,6 +78,9 @@ enum {
 
 enum { KV_MAX_BATCH = 64, KV_MAX_SEGMENTS = 64, KV_MAX_FORK = 64 };
 
+/* Size of the fixed work area of kv_attend_noalloc, in MiB. */
+#define KV_NOALLOC_SCRATCH_MB 64
+
 typedef int64_t kv_state;       /* catalog slot | generation << 32 */
 typedef struct kv_pool kv_pool; /* opaque */
 typedef void* kv_stream;        /* hipStream_t */
@@ -229,6 +232,25 @@ kv_status kv_checkpoint_load(kv_pool* pool, const char* path, kv_stream stream, 
  * new queries over all n+T keys to o [L][batch][T][Hq * dh]. */
 kv_status kv_attend(kv_pool* pool, const kv_state* states, int32_t batch, const void* x_dev,
                     int64_t T, void* o_dev, kv_stream stream);
+
+/* kv_attend for callers that cannot allocate memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid allocation): the same
+ * operation and kernels, with its work area in a fixed device array of
+ * KV_NOALLOC_SCRATCH_MB MiB that the library holds on each GPU until the
+ * process ends, instead of the pool's scratch area (the pool may have none).
+ * Calls no allocating routine on the host or the device.  The call runs in
+ * layer groups that fit the array: per layer, the query rows
+ * (batch * T * Hq * dh elements) and, for decode (T = 1), the split-key
+ * partials (batch * Hq * ceil(max keys / chunk) * (dh + 4) floats, chunks of
+ * 1024 keys, 512 for a batch of one), plus the decode plan once; a call of
+ * which not even one layer fits is KV_ERR_BUFSIZE and changes nothing.
+ * Nothing in the array needs to start at zero.  Every call on one GPU uses
+ * that GPU's array, so calls that overlap on one GPU (several pools or
+ * streams, several host threads) race: the caller orders them.
+ * KV_ERR_HIP if the array's device address could not be resolved when the
+ * pool was created.  Profiling events are not recorded for this call. */
+kv_status kv_attend_noalloc(kv_pool* pool, const kv_state* states, int32_t batch,
+                            const void* x_dev, int64_t T, void* o_dev, kv_stream stream);
 
 /* KV-Evict: order unpinned live states by score = alpha*reuse - beta*size -
  * gamma*age (ties by state id, ascending), and release them in that order

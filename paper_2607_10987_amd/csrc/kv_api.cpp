@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -20,7 +21,31 @@
 
 using namespace kvs;
 
+// Work area of kv_attend_noalloc: a fixed device array, one per GPU, held
+// until the process ends (the query rows, split-key partials and decode plan
+// of the layer group in flight).  Host code never uses its name as an
+// address: the device address is resolved per GPU (static_scratch_ptr).
+constexpr size_t kStaticScratchBytes = (size_t)KV_NOALLOC_SCRATCH_MB << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
+// Device address of `scratch` on the current GPU `device`, resolved on the
+// first call for that device (nullptr if it cannot be resolved).
+void* static_scratch_ptr(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  void* a = g_scratch_addr[device].load(std::memory_order_acquire);
+  if (a) return a;
+  if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  g_scratch_addr[device].store(a, std::memory_order_release);  // same value if two race
+  return a;
+}
 
 constexpr uint32_t kNoParent = 0xFFFFFFFFu;
 
@@ -109,6 +134,7 @@ struct kv_pool {
   int64_t P = 0;
   int device = 0;       // the GPU the pool's memory is on (current at creation)
   bool failed = false;  // a launch failed after device state changed: refuse further work
+  void* static_scratch = nullptr;  // that GPU's copy of `scratch` (kv_attend_noalloc)
   int32_t max_blocks = 0;
   char* pool = nullptr;
   char* meta = nullptr;
@@ -724,6 +750,7 @@ kv_status kv_pool_create(const kv_model_cfg* cfg, int64_t n_blocks, void* pool_d
   p->cfg = *cfg;
   p->P = n_blocks;
   p->device = device;
+  p->static_scratch = static_scratch_ptr(device);
   p->max_blocks = (int32_t)ceil_div(cfg->max_pos, cfg->block_size);
   p->pool = (char*)pool_dev;
   p->meta = (char*)meta_dev;
@@ -949,6 +976,18 @@ kv_status kv_attend(kv_pool* p, const kv_state* states, int32_t batch, const voi
                      p ? p->scratch_bytes : 0);
 }
 
+kv_status kv_attend_noalloc(kv_pool* p, const kv_state* states, int32_t batch,
+                            const void* x_dev, int64_t T, void* o_dev, kv_stream stream) {
+  if (!p) return KV_ERR_ARG;
+  if (!p->static_scratch) return KV_ERR_HIP;  // its address could not be resolved
+  // no profiling events for this call: creating them could allocate
+  const bool prof = p->prof;
+  p->prof = false;
+  const kv_status st = attend_impl(p, states, batch, x_dev, T, o_dev, stream,
+                                   (char*)p->static_scratch, kStaticScratchBytes);
+  p->prof = prof;
+  return st;
+}
 
 kv_status kv_compose(kv_pool* p, const kv_segment* segs, int32_t n, kv_stream stream,
                      kv_state* out) {

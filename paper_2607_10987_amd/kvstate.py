@@ -35,6 +35,7 @@ KV_PACK_CHECKSUM = 1
 KV_MAX_BATCH = 64
 KV_MAX_SEGMENTS = 64
 KV_MAX_FORK = 64
+KV_NOALLOC_SCRATCH_MB = 64
 
 
 class kv_model_cfg(ctypes.Structure):
@@ -93,6 +94,7 @@ _SIGS = {
     "kv_checkpoint_save": (_I32, [_P, _I64, ctypes.c_char_p, _P]),
     "kv_checkpoint_load": (_I32, [_P, ctypes.c_char_p, _P, _PI64]),
     "kv_attend": (_I32, [_P, _PI64, _I32, _P, _I64, _P, _P]),
+    "kv_attend_noalloc": (_I32, [_P, _PI64, _I32, _P, _I64, _P, _P]),
     "kv_evict": (_I32, [_P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double, _P, _PI32]),
     "kv_evict_truncate": (_I32, [_P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double, _P,
                                  _PI32, _PI32]),
@@ -314,6 +316,18 @@ def kv_attend(pool, states, x, T: int, o, stream=None):
         _check_tensor(o, pool, c.n_layers * n * T * c.n_q_heads * c.head_dim, "kv_attend o")
     arr = (ctypes.c_int64 * max(n, 1))(*[int(s) for s in states])
     _check(lib().kv_attend(pool, arr, n, _ptr(x), T, _ptr(o), _stream(stream)), "kv_attend")
+
+
+def kv_attend_noalloc(pool, states, x, T: int, o, stream=None):
+    n = len(states)
+    c = _CFGS.get(pool)
+    if c is not None:
+        _check_tensor(x, pool, n * T * c.d_model, "kv_attend_noalloc x")
+        _check_tensor(o, pool, c.n_layers * n * T * c.n_q_heads * c.head_dim,
+                      "kv_attend_noalloc o")
+    arr = (ctypes.c_int64 * max(n, 1))(*[int(s) for s in states])
+    _check(lib().kv_attend_noalloc(pool, arr, n, _ptr(x), T, _ptr(o), _stream(stream)),
+           "kv_attend_noalloc")
 
 
 def kv_evict(pool, max_allocated_blocks: int, alpha=0.0, beta=0.0, gamma=1.0, stream=None) -> int:
