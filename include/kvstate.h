@@ -333,6 +333,12 @@ typedef struct {
 } kv_profile_entry;
 kv_status kv_profile_enable(kv_pool* pool, int32_t enabled);
 kv_status kv_profile_read(kv_pool* pool, kv_profile_entry* out /* KV_KERNEL_KINDS */);
+/* The durations (ms) of the individual launches of one kernel kind recorded
+ * since the last kv_profile_read, in launch order (waits for them): up to
+ * `cap` values into out_ms, *n = how many there are.  The next
+ * kv_profile_read clears them. */
+kv_status kv_profile_launches(kv_pool* pool, int32_t kind, float* out_ms, int64_t cap,
+                              int64_t* n);
 
 /* Transfer-vs-recompute decision for a state of n_tokens tokens: the state-
  * aware scheduling rule of the paper (pi(S) = transfer iff

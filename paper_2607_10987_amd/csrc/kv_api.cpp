@@ -169,6 +169,7 @@ struct kv_pool {
   std::vector<Rec> pending;
   std::vector<hipEvent_t> spare;
   kv_profile_entry acc[KV_KERNEL_KINDS] = {};
+  std::vector<float> launch_ms[KV_KERNEL_KINDS];  // individual launches since the last read
   hipEvent_t ev() {
     hipEvent_t e = nullptr;
     if (!spare.empty()) {
@@ -1402,22 +1403,50 @@ kv_status kv_profile_enable(kv_pool* p, int32_t enabled) {
   return KV_OK;
 }
 
-kv_status kv_profile_read(kv_pool* p, kv_profile_entry* out) {
-  if (!p || !out) return KV_ERR_ARG;
-  for (auto& r : p->pending) {
-    KV_HIP(hipEventSynchronize(r.b));
+}  // extern "C"
+
+// Wait for the recorded launches and add them to the per-kind totals and lists.
+static kv_status profile_drain(kv_pool* p) {
+  size_t i = 0;
+  kv_status st = KV_OK;
+  for (; i < p->pending.size(); ++i) {
+    const auto& r = p->pending[i];
     float ms = 0.f;
-    KV_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
+      st = KV_ERR_HIP;
+      break;
+    }
     p->acc[r.kind].launches += 1;
     p->acc[r.kind].total_ms += ms;
+    p->launch_ms[r.kind].push_back(ms);
     p->spare.push_back(r.a);
     p->spare.push_back(r.b);
   }
-  p->pending.clear();
+  p->pending.erase(p->pending.begin(), p->pending.begin() + i);
+  return st;
+}
+
+extern "C" {
+
+kv_status kv_profile_read(kv_pool* p, kv_profile_entry* out) {
+  if (!p || !out) return KV_ERR_ARG;
+  KV_TRY(profile_drain(p));
   for (int k = 0; k < KV_KERNEL_KINDS; ++k) {
     out[k] = p->acc[k];
     p->acc[k] = kv_profile_entry{0, 0.0};
+    p->launch_ms[k].clear();
   }
+  return KV_OK;
+}
+
+kv_status kv_profile_launches(kv_pool* p, int32_t kind, float* out_ms, int64_t cap,
+                              int64_t* n) {
+  if (!p || !n || kind < 0 || kind >= KV_KERNEL_KINDS || cap < 0 || (cap > 0 && !out_ms))
+    return KV_ERR_ARG;
+  KV_TRY(profile_drain(p));
+  const auto& v = p->launch_ms[kind];
+  *n = (int64_t)v.size();
+  for (int64_t i = 0; i < std::min<int64_t>(cap, *n); ++i) out_ms[i] = v[(size_t)i];
   return KV_OK;
 }
 

@@ -111,6 +111,7 @@ _SIGS = {
                                 ctypes.c_double, ctypes.c_double, _P]),
     "kv_profile_enable": (_I32, [_P, _I32]),
     "kv_profile_read": (_I32, [_P, ctypes.c_void_p]),
+    "kv_profile_launches": (_I32, [_P, _I32, ctypes.POINTER(ctypes.c_float), _I64, _PI64]),
 }
 
 _lib = None
@@ -428,6 +429,18 @@ class kv_profile_entry(ctypes.Structure):
 
 def kv_profile_enable(pool, enabled: bool):
     _check(lib().kv_profile_enable(pool, 1 if enabled else 0), "kv_profile_enable")
+
+
+def kv_profile_launches(pool, kind: str):
+    """Durations (ms) of the individual launches of `kind` since the last
+    kv_profile_read, in launch order."""
+    k = KERNEL_KINDS.index(kind)
+    n = _I64()
+    _check(lib().kv_profile_launches(pool, k, None, 0, ctypes.byref(n)), "kv_profile_launches")
+    arr = (ctypes.c_float * max(n.value, 1))()
+    _check(lib().kv_profile_launches(pool, k, arr, n.value, ctypes.byref(n)),
+           "kv_profile_launches")
+    return list(arr)[:n.value]
 
 
 def kv_profile_read(pool):
