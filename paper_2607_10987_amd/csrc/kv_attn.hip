@@ -64,7 +64,11 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 
 constexpr int kDh = 128;
 constexpr int kKT = 64;             // keys per tile
-constexpr int kPW = 8;              // wavefronts per workgroup
+constexpr int kPW = 8;              // query heads x token groups per workgroup
+#ifndef KV_ATTN_HEADS_PER_WAVE
+#define KV_ATTN_HEADS_PER_WAVE 1
+#endif
+constexpr int kHeadsPerWave = KV_ATTN_HEADS_PER_WAVE;  // wavefronts: kPW / heads per wave
 constexpr int kPS = 4;              // pipeline stages
 constexpr int kPTile = kKT * kDh;   // elements of one K (or V) tile
 constexpr int kXcd = 8;             // XCDs per device
@@ -106,19 +110,22 @@ __device__ inline int xcd_remap(int id, int n) {
   return x < tall ? x * per + i : tall * per + (x - tall) * (per - 1) + i;
 }
 
-// grid (batch x query tiles x Hkv x lc, flattened), block 512.
-template <int G>
-__global__ void __launch_bounds__(64 * kPW, 1)
+// grid (batch x query tiles x Hkv x lc, flattened), block 64 * (8 / HP):
+// each wavefront computes HP query heads of one group of 32 tokens.
+template <int G, int HP>
+__global__ void __launch_bounds__(64 * (kPW / HP), 1)
 k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
             uint16_t* __restrict__ o, int l0, float qk_scale_log2) {
+  constexpr int NW = kPW / HP;      // wavefronts per workgroup
   constexpr int TG = kPW / G;       // token groups of 32
   constexpr int QT = 32 * TG;       // query tokens per workgroup
+  constexpr int CJ = 16 / NW;       // 1 KiB copies per operand, tile and wave
   __shared__ __attribute__((aligned(16))) uint16_t smem[kPS * 2 * kPTile];
   extern __shared__ int s_tbl[];    // block ids of the keys this workgroup reads
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hl = lane >> 5, col = lane & 31;
-  const int tg = wave / G, hw = wave % G;
+  const int tg = wave / (G / HP), hw = wave % (G / HP);
   const int qt_per_seq = (a.T + QT - 1) / QT;
   const int nx = a.batch * qt_per_seq;
   const int lid = xcd_remap(blockIdx.x, gridDim.x);
@@ -135,63 +142,78 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const bool q_valid = tq < a.T;
   const int key_end = min(n_keys, sd.n_before + t0 + QT);
   const int n_tiles = (key_end + kKT - 1) / kKT;
-  const int h = gk * G + hw;
+  const int h0 = gk * G + hw * HP;  // this wave's first query head
   const uint16_t* pool = (const uint16_t*)g.pool;
 
   // stage the block ids of keys [0, key_end) in LDS
   const int nbl = (key_end + g.B - 1) / g.B;
   const int32_t* trow = g.tables + (int64_t)sd.slot * g.max_blocks;
-  for (int i = tid; i < nbl; i += 64 * kPW) s_tbl[i] = trow[i];
+  for (int i = tid; i < nbl; i += 64 * NW) s_tbl[i] = trow[i];
 
-  // Q^T operand (registers for the whole loop)
-  bf16x8 qf[8];
+  // Q^T operands of the wave's heads (registers for the whole loop)
+  bf16x8 qf[HP][8];
   {
     const int row = seq * a.T + min(tq, a.T - 1);
-    const uint16_t* qp = qbuf + (((int64_t)lc * M + row) * g.Hq + h) * kDh;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) qf[ks] = *(const bf16x8*)(qp + ks * 16 + hl * 8);
+    for (int hh = 0; hh < HP; ++hh) {
+      const uint16_t* qp = qbuf + (((int64_t)lc * M + row) * g.Hq + h0 + hh) * kDh;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) settle(qf[ks]);
+      for (int ks = 0; ks < 8; ++ks) qf[hh][ks] = *(const bf16x8*)(qp + ks * 16 + hl * 8);
+    }
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) settle(qf[hh][ks]);
   }
   __syncthreads();  // s_tbl ready
 
   // Tile loads: 16 copies of 1 KiB (4 key rows of one block, as B >= 16) per
-  // operand; wave w issues copies w and w + 8 of K and of V.  Full tiles use a
-  // scalar block base; the last tile clamps rows past key_end to key_end - 1
-  // per lane (slots past the end of a state may hold anything).
+  // operand; wave w issues copies w, w + NW, ... of K and of V.  Full tiles
+  // use a scalar block base; the last tile clamps rows past key_end to
+  // key_end - 1 per lane (slots past the end of a state may hold anything).
   const int64_t koff = tile_off(g, l, 0, gk, 0), voff = tile_off(g, l, 1, gk, 0);
   const int64_t kv_gap = (voff - koff) * 2;
   const uint32_t lds0 = lds_addr(smem);
+  // Full-tile copies: scalar base = K tile of this (layer, head) in the key's
+  // block (one 32 x 32-bit product per copy) + the copy's first row in the
+  // block; per-lane offset = row within the copy + swizzled chunk, plus the
+  // K -> V distance for V.  B divides the 64 keys of a tile, so copy j's rows
+  // sit at the same place in their block in every tile, and the swizzle of
+  // row r = 4 j + lane / 16 depends on r mod 16 only, the same for every
+  // copy of a wave (j = wave + NW jj with 4 NW a multiple of 16): the offsets
+  // are loop invariants, one register each for K and V.
+  static_assert((4 * NW) % 16 == 0, "one swizzle per wave");
+  const char* pool_k = (const char*)pool + koff * 2;
+  const uint32_t blk_bytes = (uint32_t)(g.block_elems * 2);
+  const int r0 = wave * 4 + (lane >> 4);
+  const uint32_t cko = (uint32_t)((lane >> 4) * (kDh * 2) + (((lane & 15) ^ kswz(r0)) * 16));
+  const uint32_t cvo = (uint32_t)((lane >> 4) * (kDh * 2) + (((lane & 15) ^ vswz(r0)) * 16)) +
+                       (uint32_t)kv_gap;
   // block ids of the next full tile's copies, read one issue ahead
-  int nid[2];
+  int nid[CJ];
   auto fetch_ids = [&](int tile) {
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj)
-      nid[jj] = s_tbl[min((tile * kKT + (wave + jj * kPW) * 4) >> g.b_shift, nbl - 1)];
+    for (int jj = 0; jj < CJ; ++jj)
+      nid[jj] = s_tbl[min((tile * kKT + (wave + jj * NW) * 4) >> g.b_shift, nbl - 1)];
   };
   fetch_ids(0);
   auto issue = [&](int tile, int buf) {
     if ((tile + 1) * kKT <= key_end) {
       const uint32_t kl = lds0 + buf * 2 * kPTile * 2, vl = kl + kPTile * 2;
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = wave + jj * kPW;
-        const int key0 = tile * kKT + j * 4;
-        const int id = __builtin_amdgcn_readfirstlane(nid[jj]);
-        const char* kb = (const char*)pool +
-                         ((int64_t)id * g.block_elems + koff + (key0 & (g.B - 1)) * kDh) * 2;
-        const int r = j * 4 + (lane >> 4);
-        const uint32_t ko = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ kswz(r)) * 16);
-        const uint32_t vo = (lane >> 4) * (kDh * 2) + (((lane & 15) ^ vswz(r)) * 16);
-        lds_dma16_sv(kb, ko, kl + j * 1024);
-        lds_dma16_sv(kb + kv_gap, vo, vl + j * 1024);
+      for (int jj = 0; jj < CJ; ++jj) {
+        const int j = wave + jj * NW;
+        const uint32_t id = (uint32_t)__builtin_amdgcn_readfirstlane(nid[jj]);
+        const char* kb = pool_k + (uint64_t)id * blk_bytes + ((j * 4) & (g.B - 1)) * (kDh * 2);
+        lds_dma16_sv(kb, cko, kl + j * 1024);
+        lds_dma16_sv(kb, cvo, vl + j * 1024);
       }
     } else {
       uint16_t* Ks = smem + buf * 2 * kPTile;
       uint16_t* Vs = Ks + kPTile;
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = wave + jj * kPW;
+      for (int jj = 0; jj < CJ; ++jj) {
+        const int j = wave + jj * NW;
         const int r = j * 4 + (lane >> 4);
         const int key = min(tile * kKT + r, key_end - 1);
         const int64_t base = (int64_t)s_tbl[key >> g.b_shift] * g.block_elems +
@@ -202,106 +224,129 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     }
     fetch_ids(tile + 1);
   };
-  // S^T of one tile for this wave's 32 tokens
-  auto qk = [&](int buf, floatx16* sacc) {
+  // S^T of one tile for this wave's heads and 32 tokens; each K operand read
+  // from LDS feeds the products of all HP heads
+  auto qk = [&](int buf, floatx16 (*sacc)[2]) {
     const uint16_t* Ks = smem + buf * 2 * kPTile;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[kt][e] = 0.f;
+      for (int hh = 0; hh < HP; ++hh)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[hh][kt][e] = 0.f;
       const int r = kt * 32 + col;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ kswz(r)) * 8));
-        sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
+#pragma unroll
+        for (int hh = 0; hh < HP; ++hh)
+          sacc[hh][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[hh][ks], sacc[hh][kt], 0,
+                                                                 0, 0);
       }
     }
   };
 
-  floatx16 oacc[4];
+  floatx16 oacc[HP][4];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int hh = 0; hh < HP; ++hh)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) oacc[mt][e] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) oacc[hh][mt][e] = 0.f;
+  float m_run[HP], l_run[HP];
+#pragma unroll
+  for (int hh = 0; hh < HP; ++hh) {
+    m_run[hh] = -INFINITY;
+    l_run[hh] = 0.f;
+  }
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   // the step below computes QK^T of tile t + 1 before its own barrier, so
   // tile t + 1 must have been made visible one step earlier: four stages
   static_assert(kPS == 4, "stages");
-  auto wait_tiles = [](int k) {
+  auto wait_tiles = [](int k) {  // at most k tiles of this wave's copies pending
     if (k >= 2)
-      wait_vmcnt<8>();
+      wait_vmcnt<4 * CJ>();
     else if (k == 1)
-      wait_vmcnt<4>();
+      wait_vmcnt<2 * CJ>();
     else
       wait_vmcnt<0>();
   };
 
-  // softmax of one tile's scores: mask (MASKED only), running max, exp2,
-  // bf16 probabilities pf and their row sum; returns whether the max moved
-  float ps = 0.f, m_new = 0.f, m_use = 0.f;
-  bf16x8 pf[4];
-  auto softmax = [&](floatx16* sc, int tile, auto masked_c) -> bool {
+  // softmax of one tile's scores per head: mask (MASKED only), running max,
+  // exp2, bf16 probabilities pf and their row sum; moved[hh] = the max moved
+  float ps[HP], m_new[HP], m_use[HP];
+  bool moved[HP];
+  bf16x8 pf[HP][4];
+  auto softmax = [&](floatx16 (*sc)[2], int tile, auto masked_c) {
     constexpr bool MASKED = decltype(masked_c)::value;
     const int k0 = tile * kKT;
-    if constexpr (MASKED) {
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh) {
+      if constexpr (MASKED) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
+            if (kk > uq || kk >= n_keys) sc[hh][kt][e] = -INFINITY;
+          }
+      }
+      float mt_max = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kk = k0 + kt * 32 + (e >> 2) * 8 + hl * 4 + (e & 3);
-          if (kk > uq || kk >= n_keys) sc[kt][e] = -INFINITY;
+        for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sc[hh][kt][e]);
+      mt_max = max_xor32(mt_max) * qk_scale_log2;
+      m_new[hh] = mt_max > m_run[hh] + 8.f ? mt_max : m_run[hh];
+      m_use[hh] = m_new[hh] == -INFINITY ? 0.f : m_new[hh];
+      moved[hh] =
+          __builtin_amdgcn_readfirstlane((int)(__ballot(m_new[hh] != m_run[hh]) != 0)) != 0;
+      float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int hs = 0; hs < 2; ++hs) {
+          float p[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            p[j] = __builtin_amdgcn_exp2f(fmaf(sc[hh][kt][hs * 8 + j], qk_scale_log2, -m_use[hh]));
+          const uint32_t wv[4] = {cvt2(p[0], p[1]), cvt2(p[2], p[3]), cvt2(p[4], p[5]),
+                                  cvt2(p[6], p[7])};
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[0]), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[1]), ones, ps1, false);
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[2]), ones, ps0, false);
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[3]), ones, ps1, false);
+          pf[hh][kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(const uint4*)wv);
         }
+      ps[hh] = ps0 + ps1;
     }
-    float mt_max = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sc[kt][e]);
-    mt_max = max_xor32(mt_max) * qk_scale_log2;
-    m_new = mt_max > m_run + 8.f ? mt_max : m_run;
-    m_use = m_new == -INFINITY ? 0.f : m_new;
-    const bool moved = __builtin_amdgcn_readfirstlane((int)(__ballot(m_new != m_run) != 0)) != 0;
-    float ps0 = 0.f, ps1 = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int hs = 0; hs < 2; ++hs) {
-        float p[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          p[j] = __builtin_amdgcn_exp2f(fmaf(sc[kt][hs * 8 + j], qk_scale_log2, -m_use));
-        const uint32_t wv[4] = {cvt2(p[0], p[1]), cvt2(p[2], p[3]), cvt2(p[4], p[5]),
-                                cvt2(p[6], p[7])};
-        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[0]), ones, ps0, false);
-        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[1]), ones, ps1, false);
-        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[2]), ones, ps0, false);
-        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wv[3]), ones, ps1, false);
-        pf[kt * 2 + hs] = __builtin_bit_cast(bf16x8, *(const uint4*)wv);
-      }
-    ps = ps0 + ps1;
-    // pin the probabilities before the caller's rescale branch, so that the
+    // pin the probabilities before the caller's rescale branches, so that the
     // exponentials stay in the straight-line region with the QK^T products
 #pragma unroll
-    for (int i = 0; i < 4; ++i) settle(pf[i]);
-    settle(ps);
-    return moved;
-  };
-  auto finish = [&](bool moved) {
-    if (moved) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      l_run *= alpha;
+    for (int hh = 0; hh < HP; ++hh) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[mt][e] *= alpha;
+      for (int i = 0; i < 4; ++i) settle(pf[hh][i]);
+      settle(ps[hh]);
     }
-    l_run += ps;
-    m_run = m_new;
+  };
+  auto finish = [&]() {
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh) {
+      if (moved[hh]) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run[hh] - m_use[hh]);
+        l_run[hh] *= alpha;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[hh][mt][e] *= alpha;
+      }
+      l_run[hh] += ps[hh];
+      m_run[hh] = m_new[hh];
+    }
   };
   // O^T += V^T P^T for keys [16 s_lo, 16 s_hi) of one tile, V^T operands by
-  // transposed LDS reads
+  // transposed LDS reads, each feeding the products of all HP heads
   auto pv = [&](int tile, int s_lo, int s_hi) {
     const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
     const int gi = lane >> 4, li = lane & 15;
@@ -318,8 +363,11 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             KV_LDS4(Vs + key_b * kDh + ((ch ^ vswz(key_b)) * 8) + hf));
         const v4s vv[2] = {r0, r1};
-        oacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf[s4],
-                                                           oacc[mt], 0, 0, 0);
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+        for (int hh = 0; hh < HP; ++hh)
+          oacc[hh][mt] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[hh][s4], oacc[hh][mt], 0, 0, 0);
       }
     }
   };
@@ -328,20 +376,20 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   for (int st = 0; st < kPS - 1 && st < n_tiles; ++st) issue(st, st);
   wait_tiles(min(kPS - 1, n_tiles) - min(2, n_tiles));
   lds_barrier();
-  floatx16 sacc[2];
+  floatx16 sacc[HP][2];
   qk(0, sacc);
 
   // One step: QK^T of tile + 1 with the softmax of tile, then the PV product
   // of tile in two halves with the barrier between them: it makes tile + 2
   // visible for the next step and frees the buffer of tile - 1.
   auto step = [&](int tile, auto masked_c) {
-    floatx16 snext[2];
+    floatx16 snext[HP][2];
     qk((tile + 1) % kPS, snext);
-    const bool moved = softmax(sacc, tile, masked_c);
-    finish(moved);
+    softmax(sacc, tile, masked_c);
+    finish();
     pv(tile, 0, 2);
     if (tile + 2 < n_tiles) {
-      // copies of one wave complete in order, 4 per tile: tile + 2 is the
+      // copies of one wave complete in order, 2 CJ per tile: tile + 2 is the
       // newest issued.  Every read of the buffer about to be refilled (tile
       // - 1) fed a product issued earlier, so no LDS wait is needed here.
       wait_vmcnt<0>();
@@ -349,8 +397,11 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
     }
     pv(tile, 2, 4);
-    sacc[0] = snext[0];
-    sacc[1] = snext[1];
+#pragma unroll
+    for (int hh = 0; hh < HP; ++hh) {
+      sacc[hh][0] = snext[hh][0];
+      sacc[hh][1] = snext[hh][1];
+    }
   };
   const int first_q = sd.n_before + t0 + tg * 32;
   const int n_free = (t0 + tg * 32 + 31 < a.T) ? min((first_q + 1) / kKT, n_keys / kKT) : 0;
@@ -358,22 +409,29 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   int tile = 0;
   for (; tile < min(n_free, lim); ++tile) step(tile, std::false_type{});
   for (; tile < lim; ++tile) step(tile, std::true_type{});
-  finish(softmax(sacc, tile, std::true_type{}));
+  softmax(sacc, tile, std::true_type{});
+  finish();
   pv(tile, 0, 4);
 
-  const float l_tot = sum_xor32(l_run);
+  float l_tot[HP];
+#pragma unroll
+  for (int hh = 0; hh < HP; ++hh) l_tot[hh] = sum_xor32(l_run[hh]);
   if (!q_valid) return;
-  const float inv = 1.f / l_tot;
   const int row = seq * a.T + tq;
-  uint16_t* op = o + (((int64_t)l * M + row) * g.Hq + h) * kDh;
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int hh = 0; hh < HP; ++hh) {
+    const float inv = 1.f / l_tot[hh];
+    uint16_t* op = o + (((int64_t)l * M + row) * g.Hq + h0 + hh) * kDh;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int c0 = mt * 32 + q * 8 + hl * 4;
-      *(uint2*)(op + c0) = make_uint2(cvt2(oacc[mt][q * 4] * inv, oacc[mt][q * 4 + 1] * inv),
-                                      cvt2(oacc[mt][q * 4 + 2] * inv, oacc[mt][q * 4 + 3] * inv));
-    }
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c0 = mt * 32 + q * 8 + hl * 4;
+        *(uint2*)(op + c0) =
+            make_uint2(cvt2(oacc[hh][mt][q * 4] * inv, oacc[hh][mt][q * 4 + 1] * inv),
+                       cvt2(oacc[hh][mt][q * 4 + 2] * inv, oacc[hh][mt][q * 4 + 3] * inv));
+      }
+  }
 }
 
 size_t table_bytes(const PoolGeom& g, int max_keys) {
@@ -384,8 +442,11 @@ size_t table_bytes(const PoolGeom& g, int max_keys) {
 
 bool attn_mfma_ok(const PoolGeom& g, int dtype, const AppendDesc& a) {
   const int G = g.Hq / g.Hkv;
+  // 16 <= B <= 64 a power of two (B divides a 64-key tile); block bytes and
+  // the K -> V distance fit the 32-bit copy arithmetic
   return dtype == KV_DTYPE_BF16 && g.dh == kDh && (G == 4 || G == 8) && g.b_shift >= 0 &&
-         g.B >= 16 && kStaticLds + table_bytes(g, a.max_keys) <= kLdsMax;
+         g.B >= 16 && g.B <= kKT && g.block_elems * 2 < (int64_t)1 << 32 &&
+         kStaticLds + table_bytes(g, a.max_keys) <= kLdsMax;
 }
 
 hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const AppendDesc& a, void* o,
@@ -397,12 +458,13 @@ hipError_t launch_attn_prefill(const PoolGeom& g, const void* qbuf, const Append
   if (n > 0x7fffffff) return hipErrorInvalidValue;
   const float sc = 1.4426950408889634f / sqrtf((float)kDh);
   const size_t dyn = table_bytes(g, a.max_keys);
+  constexpr int HP = kHeadsPerWave;
   if (G == 4)
-    k_attn_pipe<4><<<(unsigned)n, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o,
-                                                     l0, sc);
+    k_attn_pipe<4, HP><<<(unsigned)n, 64 * (kPW / HP), dyn, s>>>(g, (const uint16_t*)qbuf, a,
+                                                                 (uint16_t*)o, l0, sc);
   else
-    k_attn_pipe<8><<<(unsigned)n, 64 * kPW, dyn, s>>>(g, (const uint16_t*)qbuf, a, (uint16_t*)o,
-                                                     l0, sc);
+    k_attn_pipe<8, HP><<<(unsigned)n, 64 * (kPW / HP), dyn, s>>>(g, (const uint16_t*)qbuf, a,
+                                                                 (uint16_t*)o, l0, sc);
   return hipGetLastError();
 }
 
