@@ -65,10 +65,11 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 constexpr int kDh = 128;
 constexpr int kKT = 64;             // keys per tile
 constexpr int kPW = 8;              // query heads x token groups per workgroup
-#ifndef KV_ATTN_HEADS_PER_WAVE
-#define KV_ATTN_HEADS_PER_WAVE 1
-#endif
-constexpr int kHeadsPerWave = KV_ATTN_HEADS_PER_WAVE;  // wavefronts: kPW / heads per wave
+// Query heads per wavefront (wavefronts per workgroup: kPW / kHeadsPerWave).
+// Two heads per wave share every K / V operand read from LDS between two
+// products, but need ~470 registers: one wave per SIMD, and the loss of the
+// second wave's overlap made it 8-20% slower (measured), so one it is.
+constexpr int kHeadsPerWave = 1;
 constexpr int kPS = 4;              // pipeline stages
 constexpr int kPTile = kKT * kDh;   // elements of one K (or V) tile
 constexpr int kXcd = 8;             // XCDs per device
