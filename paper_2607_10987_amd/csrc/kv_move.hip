@@ -6,19 +6,22 @@
 // All of them are HBM-bound streams of 16-byte vector accesses; every byte is
 // moved once.  Pack and unpack cut each (block, layer) slab of
 // 2 * Hkv * B * dh elements (64 KiB for an 8B-shaped bf16 block with B = 16)
-// into 8 KiB pieces, one per workgroup, two loads in flight per thread: many
-// small workgroups measured 8-12% faster than 32 KiB or 64 KiB pieces with 8
-// or 16 loads in flight.  Compose moves one slab per workgroup.  Streaming
-// loads (and most stores) past the caches with non-temporal accesses measured
-// 5-15% faster.
+// into 4 KiB pieces, one per workgroup of 256 threads, one 16-byte load per
+// thread: with the last-level cache flushed before each call, this measured
+// 84% of HBM peak for both on the 70B shape, against 74% / 71% for 8 KiB
+// pieces with two loads per thread (and less for 2 KiB, 16 KiB or more loads
+// in flight per thread).  Compose moves one slab per workgroup.  Streaming
+// loads and stores past the caches with non-temporal accesses measured 5-15%
+// faster (unpack's scattered block writes included, since the 4 KiB pieces).
 #include "kv_internal.h"
 
 namespace kvs {
 
 namespace {
 
-constexpr int kMoveThreads = 256;
-constexpr int kUnroll = 2;
+constexpr int kMoveThreads = 256;  // compose, copy-on-write, checksum folding
+constexpr int kPackThreads = 256;  // pack / unpack workgroups
+constexpr int kUnroll = 1;         // 16-byte loads in flight per pack / unpack thread
 
 __device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
@@ -42,7 +45,7 @@ __device__ inline uint4 ld_nt(const uint4* p) {
 
 // Bytes one workgroup moves: (block, layer) slabs are cut into pieces of
 // this size (grid z), each thread keeping kUnroll 16-byte loads in flight.
-constexpr int kPiece = kMoveThreads * kUnroll * 16;
+constexpr int kPiece = kPackThreads * kUnroll * 16;
 
 // Workgroup w of a (pieces x L x blocks) launch, piece fastest: consecutive
 // workgroups walk a block's layers and pieces in address order.
@@ -56,11 +59,10 @@ __device__ inline PieceIdx piece_idx(int pieces, int L) {
 
 // Copy piece `piece` of a slab of n16 16-byte chunks; chunk c belongs to
 // slot (c / row16) % B and is replaced by zeros when that slot is >= valid.
-// Loads are non-temporal; stores too unless PLAIN_ST (measured faster for the
-// scattered pool-block writes of unpack).  With CSUM, the thread also adds
-// the payload checksum terms of the chunks it copied (what it stores) to
-// s1, s2; base16 is the payload chunk index of the slab's chunk 0.
-template <bool PLAIN_ST, bool CSUM>
+// Loads and stores are non-temporal.  With CSUM, the thread also adds the
+// payload checksum terms of the chunks it copied (what it stores) to s1, s2;
+// base16 is the payload chunk index of the slab's chunk 0.
+template <bool CSUM>
 __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                   int piece, int n16, int row16, int B, int valid,
                                   int64_t base16, uint64_t& s1, uint64_t& s2) {
@@ -68,7 +70,7 @@ __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restri
   uint4 v[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    const int c = c0 + u * kMoveThreads;
+    const int c = c0 + u * kPackThreads;
     if (c < n16) {
       if (valid >= B || (c / row16) % B < valid) v[u] = ld_nt(src + c);
       else v[u] = make_uint4(0, 0, 0, 0);
@@ -76,10 +78,9 @@ __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restri
   }
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    const int c = c0 + u * kMoveThreads;
+    const int c = c0 + u * kPackThreads;
     if (c < n16) {
-      if (PLAIN_ST) dst[c] = v[u];
-      else st_nt(dst + c, v[u]);
+      st_nt(dst + c, v[u]);
       if (CSUM) {
         // words 4C .. 4C+3 of the payload, weights 4C+1 .. 4C+4
         const uint64_t w = (uint64_t)v[u].x + v[u].y + v[u].z + v[u].w;
@@ -94,7 +95,7 @@ __device__ inline void copy_piece(const uint4* __restrict__ src, uint4* __restri
 // Workgroup sum of the checksum terms, added to one of kSumSlots slots
 // (spread by workgroup id so that few workgroups meet on one address).
 __device__ inline void csum_commit(uint64_t s1, uint64_t s2, unsigned long long* slots) {
-  __shared__ uint64_t part[2][kMoveThreads / 64];
+  __shared__ uint64_t part[2][kPackThreads / 64];
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     s1 += __shfl_xor((unsigned long long)s1, o);
@@ -108,7 +109,7 @@ __device__ inline void csum_commit(uint64_t s1, uint64_t s2, unsigned long long*
   __syncthreads();
   if (threadIdx.x == 0) {
     uint64_t a = 0, b = 0;
-    for (int i = 0; i < kMoveThreads / 64; ++i) {
+    for (int i = 0; i < kPackThreads / 64; ++i) {
       a += part[0][i];
       b += part[1][i];
     }
@@ -121,7 +122,7 @@ __device__ inline void csum_commit(uint64_t s1, uint64_t s2, unsigned long long*
 // grid pieces x L x nblk (flattened): buffer block i, layer l  <-  pool
 // block trow[b0 + i], layer l
 template <bool CSUM>
-__global__ void __launch_bounds__(kMoveThreads)
+__global__ void __launch_bounds__(kPackThreads)
 k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t nblk,
        int32_t last_valid, char* dst, int64_t base16, unsigned long long* slots) {
   const PieceIdx pi = piece_idx(pieces, g.L);
@@ -133,8 +134,8 @@ k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t
   char* d = dst + i * block_bytes + l * layer_bytes;
   const int valid = (i == nblk - 1) ? last_valid : g.B;
   uint64_t s1 = 0, s2 = 0;
-  copy_piece<false, CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
-                          g.dh * elt / 16, g.B, valid,
+  copy_piece<CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
+                   g.dh * elt / 16, g.B, valid,
                           base16 + (i * block_bytes + l * layer_bytes) / 16, s1, s2);
   if (CSUM) csum_commit(s1, s2, slots);
 }
@@ -142,7 +143,7 @@ k_pack(PoolGeom g, int elt, int pieces, const int32_t* trow, int64_t b0, int32_t
 // grid pieces x L x nblk (flattened): pool block trow[i], layer l  <-  buffer
 // block i, layer l
 template <bool CSUM>
-__global__ void __launch_bounds__(kMoveThreads)
+__global__ void __launch_bounds__(kPackThreads)
 k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src, int64_t base16,
          unsigned long long* slots) {
   const PieceIdx pi = piece_idx(pieces, g.L);
@@ -153,8 +154,8 @@ k_unpack(PoolGeom g, int elt, int pieces, const int32_t* trow, const char* src, 
   const char* s = src + i * block_bytes + l * layer_bytes;
   char* d = (char*)g.pool + id * block_bytes + l * layer_bytes;
   uint64_t s1 = 0, s2 = 0;
-  copy_piece<true, CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
-                         g.dh * elt / 16, g.B, g.B,
+  copy_piece<CSUM>((const uint4*)s, (uint4*)d, pi.piece, (int)(layer_bytes / 16),
+                   g.dh * elt / 16, g.B, g.B,
                          base16 + (i * block_bytes + l * layer_bytes) / 16, s1, s2);
   if (CSUM) csum_commit(s1, s2, slots);
 }
@@ -461,10 +462,10 @@ hipError_t launch_pack(const PoolGeom& g, int dtype, const int32_t* trow, int64_
   const int64_t n = (int64_t)pieces * g.L * nblk;
   if (n > 0x7fffffff) return hipErrorInvalidValue;
   if (slots)
-    k_pack<true><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk, last_valid,
+    k_pack<true><<<(unsigned)n, kPackThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk, last_valid,
                                                       (char*)dst, base16, slots);
   else
-    k_pack<false><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk,
+    k_pack<false><<<(unsigned)n, kPackThreads, 0, s>>>(g, elt, pieces, trow, b0, nblk,
                                                        last_valid, (char*)dst, 0, nullptr);
   return hipGetLastError();
 }
@@ -478,10 +479,10 @@ hipError_t launch_unpack(const PoolGeom& g, int dtype, const int32_t* trow, int3
   const int64_t n = (int64_t)pieces * g.L * nblk;
   if (n > 0x7fffffff) return hipErrorInvalidValue;
   if (slots)
-    k_unpack<true><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow, (const char*)src,
+    k_unpack<true><<<(unsigned)n, kPackThreads, 0, s>>>(g, elt, pieces, trow, (const char*)src,
                                                         base16, slots);
   else
-    k_unpack<false><<<(unsigned)n, kMoveThreads, 0, s>>>(g, elt, pieces, trow,
+    k_unpack<false><<<(unsigned)n, kPackThreads, 0, s>>>(g, elt, pieces, trow,
                                                          (const char*)src, 0, nullptr);
   return hipGetLastError();
 }
