@@ -112,7 +112,7 @@ def test_layer_groups_batched_decode(gpu_available, per_group):
     chunks = -(-(n_ctx + 3) // 1024)          # keys per decode call <= n_ctx + 3
     q_layer = align256(A * shape.n_q_heads * shape.head_dim * 2)
     part_layer = align256(A * shape.n_q_heads * chunks * (shape.head_dim + 4) * 4)
-    plan = align256(chunks * A * 16) + align256(chunks * 4)
+    plan = align256(chunks * A * (16 + 64 * 4)) + align256(chunks * 4)   # unit records, counts
     scratch = plan + per_group * (q_layer + part_layer) + q_layer // 2
     tw = Twin(shape, n_blocks=200, max_pos=2304, max_states=A + 4, wl="lgdec",
               scratch_bytes=scratch)
