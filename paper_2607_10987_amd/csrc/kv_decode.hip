@@ -175,15 +175,18 @@ __device__ inline void locate_unit(const int* __restrict__ n_units, int n_chunks
   }
 }
 
-// Wait until the stage about to be read has landed: a wavefront's copies
-// complete in issue order and a stage is 2 * kKT / 4 copies, so at most
-// `ahead` newer stages may still be pending (ahead <= 2).  Memory operations
-// issued after the stage only lengthen the wait.
+// Wait until this wavefront's copies of the stage about to be read have
+// landed: a wavefront's copies complete in issue order and it issues
+// 2 * (kKT / 4) / NW copies of each stage (NW wavefronts share the copies),
+// so at most `ahead` newer stages may still be pending (ahead <= 2).  Memory
+// operations issued after the stage only lengthen the wait.
+template <int NW = 1>
 __device__ inline void wait_stage(int ahead) {
+  constexpr int per = 2 * (kKT / 4) / NW;
   if (ahead >= 2)
-    wait_vmcnt<4 * kKT / 4>();
+    wait_vmcnt<2 * per>();
   else if (ahead == 1)
-    wait_vmcnt<2 * kKT / 4>();
+    wait_vmcnt<per>();
   else
     wait_vmcnt<0>();
 }
@@ -195,10 +198,14 @@ __device__ inline void wait_stage(int ahead) {
 // block; lane j of tb = block id of the unit's block j.  Rows past the
 // unit's last key read slots of a real block; their scores are masked and
 // their V rows zeroed in LDS before use.
+// With NW > 1 wavefronts sharing the stage, wavefront w issues copies w, w +
+// NW, ... of each operand.
+template <int NW = 1>
 __device__ inline void issue_stage(const PoolGeom& g, const char* pool_kv, int64_t kv_gap, int tb,
-                                   int tile, uint32_t stage_lds, int lane) {
+                                   int tile, uint32_t stage_lds, int lane, int w = 0) {
 #pragma unroll
-  for (int j = 0; j < kKT / 4; ++j) {
+  for (int jj = 0; jj < kKT / 4 / NW; ++jj) {
+    const int j = w + jj * NW;
     const int key0 = tile * kKT + j * 4;
     const int id = __builtin_amdgcn_readlane(tb, key0 >> g.b_shift);
     const char* kb = pool_kv + ((int64_t)id * g.block_elems + (key0 & (g.B - 1)) * kDh) * 2;
@@ -514,25 +521,33 @@ struct DecodeItem {
   int tb;
 };
 
-// grid (W), block 64, every unit with one query slice (at most 32 RT query
-// vectors), at most kPersMaxChunks chunks.  Persistent: wavefront w takes
-// items w, w + W, w + 2W, ... of the list (unit, layer, KV head) in that
-// order, units in chunk order, so that the full chunks of a shared context
-// come first and the short last chunks fill the end.  The stage ring runs
+// grid (W), block 64 NW, units of at most 32 RT NW query vectors, at most
+// kPersMaxChunks chunks.  Persistent: workgroup w takes items w, w + W, w +
+// 2W, ... of the list (unit, layer, KV head) in that order, units in chunk
+// order, so that the full chunks of a shared context come first and the
+// short last chunks fill the end.  The NW wavefronts of a workgroup share one
+// LDS stage ring (each issues its share of every stage's copies; a barrier
+// per stage makes the stage visible to all and frees the slot consumed
+// before it) and each scores 32 RT of the unit's query vectors, so that a
+// deep ring and the matrix cores of several SIMDs serve the same bytes.  The ring runs
 // across items: the first stages of the next item are issued while the
-// current item's last stages are consumed, so a wavefront pays the copy
+// current item's last stages are consumed, so a workgroup pays the copy
 // latency once, not once per item.  The next item's record (read a whole
 // item ahead) and query vectors (loaded at the start of the current item)
 // are waited for only at the switch between items, the one point where the
-// compiler drains the wavefront's memory operations.
-template <int RT, int S>
-__global__ void __launch_bounds__(64)
+// compiler drains a wavefront's memory operations.
+template <int NW, int RT, int S>
+__global__ void __launch_bounds__(64 * NW)
 k_decode_pers(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
               const DecodeUnit* __restrict__ units, const int* __restrict__ n_units,
               float* __restrict__ part, int n_chunks, int l0, int lcn, float qk_scale_log2) {
   static_assert(S >= 2 && S <= 4, "stages");
+  static_assert(NW == 1 || NW == 2 || NW == 4, "wavefronts per workgroup");
   __shared__ __attribute__((aligned(16))) uint16_t smem[S * kStage];
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q0 = 32 * RT * wv;  // this wavefront's first query vector of a unit
+  const int wcp = NW == 1 ? 0 : wv;  // copy share (a constant for one wavefront)
   const int G = g.Hq / g.Hkv, b = a.batch, M = b;  // T == 1
   const uint32_t lds0 = lds_addr(smem);
   const int64_t kv_gap = (tile_off(g, 0, 1, 0, 0) - tile_off(g, 0, 0, 0, 0)) * 2;
@@ -543,7 +558,7 @@ k_decode_pers(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const int per_u = lcn * g.Hkv;
   const int n_items = total * per_u;
   int i = blockIdx.x;
-  if (i >= n_items) return;
+  if (i >= n_items) return;  // workgroup-uniform
 
   // record words of item j: lane l holds word l (header in lanes 0-3) and
   // word l + 4 (block id l)
@@ -587,7 +602,7 @@ k_decode_pers(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       settle(w1);
       make_item(w0, w1, c, lc, gk, nxt);
     }
-    load_q<RT>(g, qbuf, cur.mask, __popcll(cur.mask) * G, 0, cur.gk, cur.lc, M, lane, qf, qrow,
+    load_q<RT>(g, qbuf, cur.mask, __popcll(cur.mask) * G, q0, cur.gk, cur.lc, M, lane, qf, qrow,
                qhead);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
@@ -597,15 +612,16 @@ k_decode_pers(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
 
   int base = 0;    // stream index of cur's first stage
   int issued = 0;  // stages issued so far
-  // issue the next stage of the stream (cur's stages, then nxt's) if any
+  // issue this wavefront's share of the next stage of the stream (cur's
+  // stages, then nxt's) if any
   auto issue_next = [&]() {
     const int s = issued;
     const uint32_t sl = lds0 + (s % S) * kStage * 2;
     if (s - base < cur.n_tiles) {
-      issue_stage(g, cur.pool_kv, kv_gap, cur.tb, s - base, sl, lane);
+      issue_stage<NW>(g, cur.pool_kv, kv_gap, cur.tb, s - base, sl, lane, wcp);
       ++issued;
     } else if (has_nxt && s - base - cur.n_tiles < nxt.n_tiles) {
-      issue_stage(g, nxt.pool_kv, kv_gap, nxt.tb, s - base - cur.n_tiles, sl, lane);
+      issue_stage<NW>(g, nxt.pool_kv, kv_gap, nxt.tb, s - base - cur.n_tiles, sl, lane, wcp);
       ++issued;
     }
   };
@@ -614,29 +630,37 @@ k_decode_pers(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   float m_run[RT], l_run[RT];
   for (;;) {
     // prefetch for the switch after this item: nxt's query vectors and the
-    // record of the item after it
-    // (unconditional, so that no copy of a pending value lands before the
-    // switch: no next item loads nothing, a missing item after it re-reads
-    // the current record)
+    // record of the item after it (unconditional, so that no copy of a
+    // pending value lands before the switch: no next item loads nothing, a
+    // missing item after it re-reads the current record)
     const bool has_nn = has_nxt && i + 2 * W < n_items;
     const uint64_t qmask = has_nxt ? nxt.mask : 0;
-    load_q<RT>(g, qbuf, qmask, __popcll(qmask) * G, 0, nxt.gk, nxt.lc, M, lane, qn, qrow_n,
+    load_q<RT>(g, qbuf, qmask, __popcll(qmask) * G, q0, nxt.gk, nxt.lc, M, lane, qn, qrow_n,
                qhead_n);
     load_rec(has_nn ? i + 2 * W : i, nw0, nw1, nc, nlc, ngk);
+    // top up the ring to S - 1 stages ahead; every slot written here was
+    // consumed before the last barrier
 #pragma unroll
     for (int st = 0; st < S - 1; ++st)
       if (issued - base < S - 1) issue_next();
 
-    const int R = __popcll(cur.mask) * G;
-    const bool two = RT > 1 && R > 32;
+    const int R = __popcll(cur.mask) * G;  // the unit's query vectors
+    const bool active = q0 < R;              // wavefront-uniform
+    const bool two = RT > 1 && R - q0 > 32;
     clear_state<RT>(oacc, m_run, l_run);
     for (int t = 0; t < cur.n_tiles; ++t) {
       const int s = base + t;
-      wait_stage(issued - s - 1);
-      // the slot of stage s - 1 was consumed in the previous iteration
+      wait_stage<NW>(issued - s - 1);
+      // several wavefronts: every wavefront's copies of stage s are visible
+      // and every LDS access of stage s - 1 (reads, tail zeroing) is done, so
+      // its slot may be refilled.  One: the slot's reads fed products issued
+      // in the previous iteration, and its tail zeroing precedes the copy
+      // that refills it by a whole stage.
+      if constexpr (NW > 1) lds_barrier();
       if (issued < s + S) issue_next();
-      attend_stage<RT>(smem + (s % S) * kStage, t * kKT, cur.nk, two, qf, oacc, m_run, l_run,
-                       qk_scale_log2, lane);
+      if (NW == 1 || active)
+        attend_stage<RT>(smem + (s % S) * kStage, t * kKT, cur.nk, two, qf, oacc, m_run, l_run,
+                         qk_scale_log2, lane);
     }
     if (!has_nxt) {
       write_partials<RT>(part, g, b, cur.lc, cur.c, n_chunks, qrow, qhead, oacc, m_run, l_run,
@@ -765,9 +789,9 @@ size_t decode_scratch_bound(int64_t L, int64_t batch, int64_t Hq, int64_t max_ke
 }
 
 namespace {
-// Resident wavefronts of k_decode_pers<RT, S> on the current device: CUs x
-// workgroups per CU (bounded by LDS and registers), cached per device.
-template <int RT, int S>
+// Resident workgroups of k_decode_pers<NW, RT, S> on the current device: CUs
+// x workgroups per CU (bounded by LDS and registers), cached per device.
+template <int NW, int RT, int S>
 int pers_slots() {
   static int cache[64];
   int dev = 0;
@@ -776,11 +800,23 @@ int pers_slots() {
     int cus = 0, per = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per, reinterpret_cast<const void*>(&k_decode_pers<RT, S>), 64, 0) != hipSuccess)
+            &per, reinterpret_cast<const void*>(&k_decode_pers<NW, RT, S>), 64 * NW, 0) !=
+            hipSuccess)
       return 256;
     cache[dev] = std::max(1, cus * per);
   }
   return cache[dev];
+}
+}  // namespace
+
+namespace {
+template <int NW, int RT, int S>
+void launch_pers(const PoolGeom& g, const void* qbuf, const AppendDesc& a, const DecodeUnit* units,
+                 const int* n_units, float* part, int nch, int l0, int lc, float sc,
+                 int64_t items_max, hipStream_t s) {
+  const int w = (int)std::min<int64_t>(pers_slots<NW, RT, S>(), items_max);
+  k_decode_pers<NW, RT, S><<<w, 64 * NW, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
+                                             nch, l0, lc, sc);
 }
 }  // namespace
 
@@ -801,25 +837,21 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   const int ns = (a.batch * G + 63) / 64;  // query slices of 64 vectors
   if (ns > 1) slots = (slots + 7) / 8 * 8;
   dim3 grid(slots * ns, g.Hkv, lc);
-  // One query slice and at most kPersMaxChunks chunks: the persistent form,
-  // one wavefront per resident slot, each walking its list of (unit, layer,
-  // KV head) items.  One query tile: four 16 KiB stages per wave (three in
-  // flight, two waves per CU), 2% faster than three stages (three waves per
-  // CU); two query tiles: two stages (four waves per CU, one per SIMD), 7%
-  // and 30% faster than three and four stages.  Otherwise (query slices) one
-  // wavefront per (unit, slice, KV head, layer): three stages for one query
-  // tile, two for two (15% faster than three).
-  if (ns == 1 && nch <= kPersMaxChunks) {
+  // At most 128 query vectors per unit and kPersMaxChunks chunks: the
+  // persistent form, one workgroup of 1, 2 or 4 wavefronts (32 query vectors
+  // each) per resident slot, each walking its list of (unit, layer, KV head)
+  // items.  Otherwise one wavefront per (unit, query slice of 64 vectors, KV
+  // head, layer): three stages for one query tile, two for two (15% faster
+  // than three).
+  const int vec = a.batch * G;
+  if (vec <= 128 && nch <= kPersMaxChunks) {
     const int64_t items_max = (int64_t)nch * a.batch * lc * g.Hkv;
-    if (a.batch * G <= 32) {
-      const int w = (int)std::min<int64_t>(pers_slots<1, 4>(), items_max);
-      k_decode_pers<1, 4><<<w, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part, nch,
-                                           l0, lc, sc);
-    } else {
-      const int w = (int)std::min<int64_t>(pers_slots<2, 2>(), items_max);
-      k_decode_pers<2, 2><<<w, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part, nch,
-                                           l0, lc, sc);
-    }
+    if (vec <= 32)
+      launch_pers<1, 1, 4>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
+    else if (vec <= 64)
+      launch_pers<1, 2, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
+    else
+      launch_pers<4, 1, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
   } else if (a.batch * G <= 32)
     k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, ck, l0, sc, 1);
