@@ -9,7 +9,8 @@ oracle's re-rotation of the stored source keys):
 * layer groups: a scratch area smaller than a call needs for all layers, so
   that the call runs layer group by layer group (prefill, append, batched
   decode with its work plan reused across groups);
-* decode batches beyond 64 query vectors per KV head (query slices);
+* decode batches beyond 64 query vectors per KV head (four wavefronts per
+  unit, query slices) and contexts of more than 256 key chunks;
 * a Llama-scale RoPE base (5e5) at positions near 35k and compositions that
   shift segments by about +-30k positions;
 * the projection kernels for d_model values and row counts the 8B / 70B
@@ -133,9 +134,10 @@ def test_layer_groups_batched_decode(gpu_available, per_group):
 
 def test_decode_query_slices(gpu_available):
     """Decode batches with more than 64 query vectors per KV head stay on the
-    MFMA decode path (the merge kernel runs), split into query slices: 32
-    and 64 agents x 4 query heads at the 8B head shape, 17 agents x 8 query
-    heads at the 70B head shape."""
+    MFMA decode path (the merge kernel runs): 32 agents x 4 query heads at
+    the 8B head shape (128 vectors: four wavefronts of 32 share a unit's
+    stages), 64 agents x 4 query heads and 17 agents x 8 query heads at the
+    70B head shape (more than 128: query slices of 64 vectors)."""
     shape = shape8b(L=2)
     tw = Twin(shape, n_blocks=260, max_pos=1200, max_states=70, wl="slices", check_kv=False)
     hdr, ohdr, buf, pay = tw.synthetic_transfer(66, 1050, 0, tag=2)   # 1050 keys: 2 chunks
@@ -222,4 +224,25 @@ def test_compose_bf16_head_dim_96(gpu_available):
     nb = kv.kv_state_info(tw.gpu.h, c)["n_blocks"]
     hdr, ohdr, buf, pay = tw.pack(c, 0, nb)
     tw.unpack(hdr, ohdr, buf, pay, rerotated_from=c)
+    tw.close()
+
+
+def test_decode_many_chunks(gpu_available):
+    """Decode over a 139990-token context (a seeded payload unpacked into the
+    pool; one KV head of 128 channels, so the oracle stays small): a batch of
+    one cuts it into 274 chunks of 512 keys, more than the persistent kernel
+    indexes, so the per-unit stream kernel runs; batches of 2 and 3 forked
+    agents cut it into 137 chunks of 1024 keys, which the persistent kernel
+    finds through its unit counts in three registers per lane."""
+    shape = synth.ModelShape("long", 2, 256, 4, 1, 128, 16, "bf16")
+    n_ctx = 139990
+    nb = -(-n_ctx // shape.block_size)
+    tw = Twin(shape, n_blocks=nb + 64, max_pos=n_ctx + 64, max_states=8, wl="long",
+              check_kv=False)
+    hdr, ohdr, buf, pay = tw.synthetic_transfer(nb, n_ctx, 0, tag=3)
+    root = tw.unpack(hdr, ohdr, buf, pay)
+    tw.attend([root], 1)                    # 139991 keys, batch 1: 274 chunks
+    kids = tw.fork(root, 3)
+    tw.attend(kids[:2], 1)                  # batch 2: 137 chunks
+    tw.attend(kids, 1)                      # mixed histories, batch 3
     tw.close()
