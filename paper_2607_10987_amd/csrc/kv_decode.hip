@@ -20,15 +20,16 @@
 // a query with the usual log-sum-exp rescaling.  A unit's record carries its
 // block ids, so a wavefront can start copying after one read of it.
 //
-// k_decode_pers (units of at most 64 query vectors, the usual case) is
-// persistent: one wavefront per resident slot walks a static list of (unit,
-// layer, KV head) items, largest first, and keeps its stage ring running
-// across items, so the copy latency is paid once per wavefront rather than
-// once per item (a stream-only probe that read every unit twice without a
-// restart took 1.9x, not 2x, the time of one pass).  k_decode_stream takes
-// units with more query vectors (e.g. 32 members x 4 query heads), split into
-// query slices of 64 vectors, each a wavefront of its own that streams the
-// same keys; the slices of a unit are launched on one XCD, so the later ones
+// k_decode_pers is persistent: one workgroup per resident slot walks a
+// static list of (unit, layer, KV head) items, largest first, and keeps its
+// stage ring running across items, so the copy latency is paid once per
+// workgroup rather than once per item (a stream-only probe that read every
+// unit twice without a restart took 1.9x, not 2x, the time of one pass); a
+// switch between items still costs about one refill of the ring.  It takes
+// units of 65 to 128 query vectors (four wavefronts sharing the ring) and
+// units of at most 64 while each slot has few items.  k_decode_stream runs
+// one wavefront per (unit, query slice of 64 vectors, KV head, layer) for
+// the rest; the slices of a unit are launched on one XCD, so the later ones
 // find the keys in its L2.
 #include <algorithm>
 
@@ -810,6 +811,10 @@ int pers_slots() {
 }  // namespace
 
 namespace {
+// Items per resident slot up to which the persistent form is used (units of
+// at most 64 query vectors).
+constexpr int64_t kPersItemsPerSlot = 16;
+
 template <int NW, int RT, int S>
 void launch_pers(const PoolGeom& g, const void* qbuf, const AppendDesc& a, const DecodeUnit* units,
                  const int* n_units, float* part, int nch, int l0, int lc, float sc,
@@ -837,21 +842,28 @@ hipError_t launch_decode_attn(const PoolGeom& g, const void* qbuf, const AppendD
   const int ns = (a.batch * G + 63) / 64;  // query slices of 64 vectors
   if (ns > 1) slots = (slots + 7) / 8 * 8;
   dim3 grid(slots * ns, g.Hkv, lc);
-  // At most 128 query vectors per unit and kPersMaxChunks chunks: the
-  // persistent form, one workgroup of 1, 2 or 4 wavefronts (32 query vectors
-  // each) per resident slot, each walking its list of (unit, layer, KV head)
-  // items.  Otherwise one wavefront per (unit, query slice of 64 vectors, KV
-  // head, layer): three stages for one query tile, two for two (15% faster
-  // than three).
+  // Units of 65 to 128 query vectors (at most kPersMaxChunks chunks): the
+  // persistent form with four wavefronts of 32 vectors per workgroup sharing
+  // one stage ring (32 agents x 4 query heads, 8192 keys, 32 layers: 341
+  // against 496 us as query slices).  At most 64 vectors: the persistent form
+  // (one wavefront per resident slot) only while each slot takes at most
+  // kPersItemsPerSlot items (counting every (chunk, member) as a unit, an
+  // upper bound), since each switch between items costs about one refill of
+  // the ring; with more (batch one over a long context, 80 layers) the
+  // per-unit kernel, whose start-up other wavefronts of the CU cover, is 3-5%
+  // faster, with fewer (fork4-8b decode) 4-5% slower.  Otherwise one
+  // wavefront per (unit, query slice of 64 vectors, KV head, layer): three
+  // stages for one query tile, two for two (15% faster than three).
   const int vec = a.batch * G;
-  if (vec <= 128 && nch <= kPersMaxChunks) {
-    const int64_t items_max = (int64_t)nch * a.batch * lc * g.Hkv;
-    if (vec <= 32)
-      launch_pers<1, 1, 4>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
-    else if (vec <= 64)
-      launch_pers<1, 2, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
-    else
-      launch_pers<4, 1, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
+  const int64_t items_max = (int64_t)nch * a.batch * lc * g.Hkv;
+  if (vec > 64 && vec <= 128 && nch <= kPersMaxChunks) {
+    launch_pers<4, 1, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
+  } else if (vec <= 32 && nch <= kPersMaxChunks &&
+             items_max <= (int64_t)kPersItemsPerSlot * pers_slots<1, 1, 3>()) {
+    launch_pers<1, 1, 3>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
+  } else if (vec > 32 && vec <= 64 && nch <= kPersMaxChunks &&
+             items_max <= (int64_t)kPersItemsPerSlot * pers_slots<1, 2, 2>()) {
+    launch_pers<1, 2, 2>(g, qbuf, a, units, n_units, part, nch, l0, lc, sc, items_max, s);
   } else if (a.batch * G <= 32)
     k_decode_stream<1, 3><<<grid, 64, 0, s>>>(g, (const uint16_t*)qbuf, a, units, n_units, part,
                                               nch, ck, l0, sc, 1);
