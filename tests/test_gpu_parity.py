@@ -329,10 +329,10 @@ def test_bf16_ragged_edges(gpu_available):
     kernel: a one-token state (decode-path kernels over a single key),
     prefills of 33 and 300 tokens (partial 256-row projection and 64-token
     attention tiles), decode batches of 3, 5 and 17 (17 agents x 4 query heads
-    = 68 query vectors per KV head: two query slices of the MFMA decode path,
-    and 17 token rows for the projection), appends of 2 x 33 rows and of 70
-    rows behind 301 cached tokens, a three-segment compose and a pack / unpack
-    of the result."""
+    = 68 query vectors per KV head: four wavefronts of the MFMA decode path
+    share each unit, and 17 token rows for the projection), appends of 2 x 33
+    rows and of 70 rows behind 301 cached tokens, a three-segment compose and
+    a pack / unpack of the result."""
     base = synth.LLAMA8B_SHAPE
     shape = synth.ModelShape("8b-l2", 2, base.d_model, base.n_q_heads, base.n_kv_heads,
                              base.head_dim, base.block_size, "bf16")
