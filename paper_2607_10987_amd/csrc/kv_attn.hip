@@ -231,18 +231,15 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     const uint16_t* Ks = smem + buf * 2 * kPTile;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-      for (int hh = 0; hh < HP; ++hh)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[hh][kt][e] = 0.f;
       const int r = kt * 32 + col;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ kswz(r)) * 8));
+        // the first product of a chain takes a literal zero accumulator
 #pragma unroll
         for (int hh = 0; hh < HP; ++hh)
-          sacc[hh][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[hh][ks], sacc[hh][kt], 0,
-                                                                 0, 0);
+          sacc[hh][kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              kf, qf[hh][ks], ks == 0 ? floatx16{} : sacc[hh][kt], 0, 0, 0);
       }
     }
   };
@@ -380,13 +377,15 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   floatx16 sacc[HP][2];
   qk(0, sacc);
 
-  // One step: QK^T of tile + 1 with the softmax of tile, then the PV product
-  // of tile in two halves with the barrier between them: it makes tile + 2
-  // visible for the next step and frees the buffer of tile - 1.
-  auto step = [&](int tile, auto masked_c) {
-    floatx16 snext[HP][2];
-    qk((tile + 1) % kPS, snext);
-    softmax(sacc, tile, masked_c);
+  // One step: QK^T of tile + 1 (into snx) with the softmax of tile (scores
+  // in scur), then the PV product of tile in two halves with the barrier
+  // between them: it makes tile + 2 visible for the next step and frees the
+  // buffer of tile - 1.  Steps run in pairs that swap the two score sets, so
+  // no scores are copied between registers.
+  floatx16 sB[HP][2];
+  auto step = [&](int tile, floatx16 (*scur)[2], floatx16 (*snx)[2], auto masked_c) {
+    qk((tile + 1) % kPS, snx);
+    softmax(scur, tile, masked_c);
     finish();
     pv(tile, 0, 2);
     if (tile + 2 < n_tiles) {
@@ -398,18 +397,31 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
     }
     pv(tile, 2, 4);
+  };
+  // a step left over after the pairs: its next scores become sacc
+  auto step_copy = [&](int tile, auto masked_c) {
+    step(tile, sacc, sB, masked_c);
 #pragma unroll
     for (int hh = 0; hh < HP; ++hh) {
-      sacc[hh][0] = snext[hh][0];
-      sacc[hh][1] = snext[hh][1];
+      sacc[hh][0] = sB[hh][0];
+      sacc[hh][1] = sB[hh][1];
     }
   };
   const int first_q = sd.n_before + t0 + tg * 32;
   const int n_free = (t0 + tg * 32 + 31 < a.T) ? min((first_q + 1) / kKT, n_keys / kKT) : 0;
   const int lim = n_tiles - 1;
+  const int nf = min(n_free, lim);
   int tile = 0;
-  for (; tile < min(n_free, lim); ++tile) step(tile, std::false_type{});
-  for (; tile < lim; ++tile) step(tile, std::true_type{});
+  for (; tile + 1 < nf; tile += 2) {
+    step(tile, sacc, sB, std::false_type{});
+    step(tile + 1, sB, sacc, std::false_type{});
+  }
+  if (tile < nf) step_copy(tile++, std::false_type{});
+  for (; tile + 1 < lim; tile += 2) {
+    step(tile, sacc, sB, std::true_type{});
+    step(tile + 1, sB, sacc, std::true_type{});
+  }
+  if (tile < lim) step_copy(tile++, std::true_type{});
   softmax(sacc, tile, std::true_type{});
   finish();
   pv(tile, 0, 4);
