@@ -23,7 +23,11 @@
 // Staging: K and V tiles stream straight from the pool into LDS
 // (global_load_lds_dwordx4) through 4 stages as unpadded 256-byte key rows
 // whose 16-byte chunks are permuted per row (kswz, vswz) so that the reads
-// below hit every bank group evenly.  V stays key major; its operand (4 consecutive keys of one channel per half) is read
+// below hit every bank group evenly.  The four K stages come first in LDS,
+// then the four V stages (16 KiB each), so that every operand read is one
+// loop-invariant per-lane address register plus an immediate offset (stage,
+// key group) below 64 KiB when the stage is known at compile time.  V stays
+// key major; its operand (4 consecutive keys of one channel per half) is read
 // with ds_read_b64_tr_b16: within each group of 16 lanes, lane i addressing
 // row key0 + i / 4, channels c0 + 4 (i % 4) .. + 3 receives keys
 // key0 .. key0 + 3 of channel c0 + i.
@@ -36,7 +40,8 @@
 // the rare accumulator rescale, placed after the exponentials): the last tile
 // is handled after the loop, and the tiles that no query of the wave masks
 // run in a loop of their own without mask code (the mask is applied only on
-// the causal diagonal and on ragged ends).  The one workgroup barrier per
+// the causal diagonal and on ragged ends), unrolled by the four stages so
+// that each step's stage is a constant.  The one workgroup barrier per
 // tile sits between the two PV halves, so a wave meets it with products
 // still to issue; it makes tile t + 2 visible and frees the buffer of tile
 // t - 1 for the copies of tile t + 3.  The block ids of a tile's copies are
@@ -200,7 +205,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   fetch_ids(0);
   auto issue = [&](int tile, int buf) {
     if ((tile + 1) * kKT <= key_end) {
-      const uint32_t kl = lds0 + buf * 2 * kPTile * 2, vl = kl + kPTile * 2;
+      const uint32_t kl = lds0 + buf * kPTile * 2, vl = kl + kPS * kPTile * 2;
 #pragma unroll
       for (int jj = 0; jj < CJ; ++jj) {
         const int j = wave + jj * NW;
@@ -210,8 +215,8 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         lds_dma16_sv(kb, cvo, vl + j * 1024);
       }
     } else {
-      uint16_t* Ks = smem + buf * 2 * kPTile;
-      uint16_t* Vs = Ks + kPTile;
+      uint16_t* Ks = smem + buf * kPTile;
+      uint16_t* Vs = Ks + kPS * kPTile;
 #pragma unroll
       for (int jj = 0; jj < CJ; ++jj) {
         const int j = wave + jj * NW;
@@ -225,16 +230,44 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
     }
     fetch_ids(tile + 1);
   };
+  // Per-lane LDS byte addresses of the operand reads in stage 0: K for each
+  // k-substep ks of the first 32 keys (the second 32 keys are 8 KiB further,
+  // and kswz(32 + r) = kswz(r)); V for each 32-channel block mt and key half
+  // of the first 16 keys (key group s4 is 4 KiB further, and vswz is the same
+  // for keys r and r + 16 s4).  settle() keeps the compiler from splitting
+  // them into more registers.
+  uint32_t kof[8], vof[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) {
+    kof[ks] = lds0 + (uint32_t)(col * kDh + (((ks * 2 + hl) ^ kswz(col)) * 8)) * 2;
+    settle(kof[ks]);
+  }
+  {
+    const int gi = lane >> 4, li = lane & 15;
+    const int key_a = (gi >> 1) * 4 + (li >> 2);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int dc = mt * 32 + (gi & 1) * 16 + (li & 3) * 4;
+      const int ch = dc >> 3, hf = (dc & 7);
+#pragma unroll
+      for (int ab = 0; ab < 2; ++ab) {
+        const int key = key_a + ab * 8;
+        vof[mt * 2 + ab] = lds0 + kPS * kPTile * 2 +
+                           (uint32_t)(key * kDh + ((ch ^ vswz(key)) * 8) + hf) * 2;
+        settle(vof[mt * 2 + ab]);
+      }
+    }
+  }
   // S^T of one tile for this wave's heads and 32 tokens; each K operand read
   // from LDS feeds the products of all HP heads
   auto qk = [&](int buf, floatx16 (*sacc)[2]) {
-    const uint16_t* Ks = smem + buf * 2 * kPTile;
+    const uint32_t kb = buf * kPTile * 2;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      const int r = kt * 32 + col;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *(const bf16x8*)(Ks + r * kDh + (((ks * 2 + hl) ^ kswz(r)) * 8));
+        const bf16x8 kf =
+            *(const __attribute__((address_space(3))) bf16x8*)(kof[ks] + kb + kt * 32 * kDh * 2);
         // the first product of a chain takes a literal zero accumulator
 #pragma unroll
         for (int hh = 0; hh < HP; ++hh)
@@ -343,23 +376,19 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       m_run[hh] = m_new[hh];
     }
   };
-  // O^T += V^T P^T for keys [16 s_lo, 16 s_hi) of one tile, V^T operands by
-  // transposed LDS reads, each feeding the products of all HP heads
-  auto pv = [&](int tile, int s_lo, int s_hi) {
-    const uint16_t* Vs = smem + (tile % kPS) * 2 * kPTile + kPTile;
-    const int gi = lane >> 4, li = lane & 15;
+  // O^T += V^T P^T for keys [16 s_lo, 16 s_hi) of the tile in stage sb, V^T
+  // operands by transposed LDS reads, each feeding the products of all HP heads
+  auto pv = [&](int sb, int s_lo, int s_hi) {
+    const uint32_t vb = sb * kPTile * 2;
 #pragma unroll
     for (int s4 = s_lo; s4 < s_hi; ++s4) {
-      const int key_a = s4 * 16 + (gi >> 1) * 4 + (li >> 2);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        const int dc = mt * 32 + (gi & 1) * 16 + (li & 3) * 4;
-        const int ch = dc >> 3, hf = (dc & 7);
+        const uint32_t so = vb + s4 * 16 * kDh * 2;
         const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_a * kDh + ((ch ^ vswz(key_a)) * 8) + hf));
-        const int key_b = key_a + 8;
+            KV_LDS4(vof[mt * 2] + so));
         const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            KV_LDS4(Vs + key_b * kDh + ((ch ^ vswz(key_b)) * 8) + hf));
+            KV_LDS4(vof[mt * 2 + 1] + so));
         const v4s vv[2] = {r0, r1};
         const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
 #pragma unroll
@@ -381,26 +410,26 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   // in scur), then the PV product of tile in two halves with the barrier
   // between them: it makes tile + 2 visible for the next step and frees the
   // buffer of tile - 1.  Steps run in pairs that swap the two score sets, so
-  // no scores are copied between registers.
+  // no scores are copied between registers.  sb = the stage of tile.
   floatx16 sB[HP][2];
-  auto step = [&](int tile, floatx16 (*scur)[2], floatx16 (*snx)[2], auto masked_c) {
-    qk((tile + 1) % kPS, snx);
+  auto step = [&](int tile, int sb, floatx16 (*scur)[2], floatx16 (*snx)[2], auto masked_c) {
+    qk((sb + 1) % kPS, snx);
     softmax(scur, tile, masked_c);
     finish();
-    pv(tile, 0, 2);
+    pv(sb, 0, 2);
     if (tile + 2 < n_tiles) {
       // copies of one wave complete in order, 2 CJ per tile: tile + 2 is the
       // newest issued.  Every read of the buffer about to be refilled (tile
       // - 1) fed a product issued earlier, so no LDS wait is needed here.
       wait_vmcnt<0>();
       barrier_only();
-      if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (tile + kPS - 1) % kPS);
+      if (tile + kPS - 1 < n_tiles) issue(tile + kPS - 1, (sb + kPS - 1) % kPS);
     }
-    pv(tile, 2, 4);
+    pv(sb, 2, 4);
   };
   // a step left over after the pairs: its next scores become sacc
   auto step_copy = [&](int tile, auto masked_c) {
-    step(tile, sacc, sB, masked_c);
+    step(tile, tile % kPS, sacc, sB, masked_c);
 #pragma unroll
     for (int hh = 0; hh < HP; ++hh) {
       sacc[hh][0] = sB[hh][0];
@@ -412,19 +441,25 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   const int lim = n_tiles - 1;
   const int nf = min(n_free, lim);
   int tile = 0;
+  for (; tile + 3 < nf; tile += 4) {
+    step(tile, 0, sacc, sB, std::false_type{});
+    step(tile + 1, 1, sB, sacc, std::false_type{});
+    step(tile + 2, 2, sacc, sB, std::false_type{});
+    step(tile + 3, 3, sB, sacc, std::false_type{});
+  }
   for (; tile + 1 < nf; tile += 2) {
-    step(tile, sacc, sB, std::false_type{});
-    step(tile + 1, sB, sacc, std::false_type{});
+    step(tile, tile % kPS, sacc, sB, std::false_type{});
+    step(tile + 1, (tile + 1) % kPS, sB, sacc, std::false_type{});
   }
   if (tile < nf) step_copy(tile++, std::false_type{});
   for (; tile + 1 < lim; tile += 2) {
-    step(tile, sacc, sB, std::true_type{});
-    step(tile + 1, sB, sacc, std::true_type{});
+    step(tile, tile % kPS, sacc, sB, std::true_type{});
+    step(tile + 1, (tile + 1) % kPS, sB, sacc, std::true_type{});
   }
   if (tile < lim) step_copy(tile++, std::true_type{});
   softmax(sacc, tile, std::true_type{});
   finish();
-  pv(tile, 0, 4);
+  pv(tile % kPS, 0, 4);
 
   float l_tot[HP];
 #pragma unroll
