@@ -83,10 +83,14 @@ constexpr size_t kStaticLds = (size_t)kPS * 2 * kPTile * 2;
 
 // Reductions over lanes l and l ^ 32 (the two halves of a token's keys) with
 // v_permlane32_swap, which leaves v[l % 32] and v[l % 32 + 32] in every lane.
-__device__ inline float max_xor32(float v) {
+// max_xor32_scaled returns max(v, v of lane l ^ 32) * c for c > 0; scaling
+// both swapped values before the max makes them results of arithmetic, which
+// the compiler knows are not signalling NaNs, so it adds no quieting
+// instructions around the max.
+__device__ inline float max_xor32_scaled(float v, float c) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return fmaxf(__uint_as_float(r[0]) * c, __uint_as_float(r[1]) * c);
 }
 __device__ inline float sum_xor32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
@@ -305,8 +309,11 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
   };
 
   // softmax of one tile's scores per head: mask (MASKED only), running max,
-  // exp2, bf16 probabilities pf and their row sum; moved[hh] = the max moved
-  float ps[HP], m_new[HP], m_use[HP];
+  // exp2, bf16 probabilities pf and their row sum; moved[hh] = the max moved.
+  // m_thr = m_run + 8, updated with m_run.
+  float ps[HP], m_new[HP], m_use[HP], m_thr[HP];
+#pragma unroll
+  for (int hh = 0; hh < HP; ++hh) m_thr[hh] = -INFINITY;
   bool moved[HP];
   bf16x8 pf[HP][4];
   auto softmax = [&](floatx16 (*sc)[2], int tile, auto masked_c) {
@@ -328,11 +335,10 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) mt_max = fmaxf(mt_max, sc[hh][kt][e]);
-      mt_max = max_xor32(mt_max) * qk_scale_log2;
-      m_new[hh] = mt_max > m_run[hh] + 8.f ? mt_max : m_run[hh];
+      mt_max = max_xor32_scaled(mt_max, qk_scale_log2);
+      m_new[hh] = mt_max > m_thr[hh] ? mt_max : m_run[hh];
       m_use[hh] = m_new[hh] == -INFINITY ? 0.f : m_new[hh];
-      moved[hh] =
-          __builtin_amdgcn_readfirstlane((int)(__ballot(m_new[hh] != m_run[hh]) != 0)) != 0;
+      moved[hh] = __ballot(m_new[hh] != m_run[hh]) != 0;
       float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
@@ -371,6 +377,7 @@ k_attn_pipe(PoolGeom g, const uint16_t* __restrict__ qbuf, AppendDesc a,
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
           for (int e = 0; e < 16; ++e) oacc[hh][mt][e] *= alpha;
+        m_thr[hh] = m_new[hh] + 8.f;
       }
       l_run[hh] += ps[hh];
       m_run[hh] = m_new[hh];
